@@ -1,0 +1,274 @@
+"""CPU oracle for the two-dimensional KV-cache migration of ReMP (Section 3.4).
+
+TEST INFRASTRUCTURE.  Only the test suite, the smoke check and the benchmark's
+CPU-baseline leg may import or run this module.  It shares no code with the
+HIP library or its Python binding and imports neither.
+
+What it computes is the plain definition the migration has to reach
+(Section 3.4.1, logical KV cache model): element KV[l, b, h] held by
+rank(l, h, T_old) must end up, unchanged, on rank(l, h, T_new).  The oracle
+does not run the paper's plan construction (Algorithm 1); it materialises the
+logical slice of each (sequence, layer) from the old shards and writes it into
+the new shards, one slice at a time, in NumPy.
+
+Readings of points the paper leaves open (each one is listed in the design doc):
+
+* ownership: pp_owner(l, PP) = l // (L / PP) (equal contiguous layer ranges),
+  tp_owner(h, TP) = h // (H / TP) (equal contiguous head ranges) and
+  rank(pp, tp) = pp * TP + tp;  L % PP == 0 and H % TP == 0 are required;
+* paged storage of a rank: per global layer it owns, K and V arrays of shape
+  [num_blocks, block_size, H / TP, head_dim]; token t of sequence s sits in
+  block table[s][t // block_size], slot t % block_size; only live tokens
+  (t < n_s) are payload;
+* the block mapping across the switch is the caller's new block tables (the
+  "deterministic block remapping" of Section 3.4.5); the new block size may
+  differ from the old one;
+* K and V are two arrays moved identically;
+* staging, the contiguous buffer an old rank r fills for a new rank q: the
+  (r, q) slices in ascending layer order, each slice laid out as
+  [kv][token of all sequences, sequence-major][head in the overlap][head_dim].
+
+Array conventions used throughout:
+* pools: {rank: {global layer: ndarray [2, num_blocks, block_size, H_loc, D]}}
+  (axis 0 is K=0 / V=1), unsigned integers of the element width;
+* tables: synthkv.BlockTables (or any object with seq_lens, row(s),
+  block_size, num_blocks).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, Iterable, List, Optional, Tuple
+
+import numpy as np
+
+
+# ---------------------------------------------------------------------------
+# topology and ownership (Section 3.4.1)
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class Topology:
+    tp: int
+    pp: int
+
+    @property
+    def world(self) -> int:
+        return self.tp * self.pp
+
+
+def check_divisible(topo: Topology, L: int, H: int) -> None:
+    if topo.tp < 1 or topo.pp < 1:
+        raise ValueError("TP and PP must be positive")
+    if L % topo.pp or H % topo.tp:
+        raise ValueError(f"(TP={topo.tp}, PP={topo.pp}) does not divide L={L}, H={H}")
+
+
+def pp_owner(l: int, topo: Topology, L: int) -> int:
+    """Pipeline stage that holds layer l."""
+    return l // (L // topo.pp)
+
+
+def tp_owner(h: int, topo: Topology, H: int) -> int:
+    """Tensor-parallel rank that holds KV head h."""
+    return h // (H // topo.tp)
+
+
+def rank_of(pp: int, tp: int, topo: Topology) -> int:
+    """Global rank of (pipeline stage, tensor rank)."""
+    return pp * topo.tp + tp
+
+
+def owner(l: int, h: int, topo: Topology, L: int, H: int) -> int:
+    """rank(l, h, T) of Section 3.4.1."""
+    return rank_of(pp_owner(l, topo, L), tp_owner(h, topo, H), topo)
+
+
+def stage_of_rank(r: int, topo: Topology) -> Tuple[int, int]:
+    return r // topo.tp, r % topo.tp
+
+
+def layers_of(r: int, topo: Topology, L: int) -> range:
+    p, _ = stage_of_rank(r, topo)
+    per = L // topo.pp
+    return range(p * per, (p + 1) * per)
+
+
+def heads_of(r: int, topo: Topology, H: int) -> range:
+    _, t = stage_of_rank(r, topo)
+    per = H // topo.tp
+    return range(t * per, (t + 1) * per)
+
+
+def pair_slices(old: Topology, new: Topology, L: int, H: int) -> Dict[Tuple[int, int], Tuple[List[int], List[int]]]:
+    """For each (old rank r, new rank q) that exchanges data: (layers, heads).
+
+    By definition: group every (l, h) by (rank(l,h,T_old), rank(l,h,T_new)).
+    """
+    check_divisible(old, L, H)
+    check_divisible(new, L, H)
+    groups: Dict[Tuple[int, int], Tuple[set, set]] = {}
+    for l in range(L):
+        for h in range(H):
+            key = (owner(l, h, old, L, H), owner(l, h, new, L, H))
+            ls, hs = groups.setdefault(key, (set(), set()))
+            ls.add(l)
+            hs.add(h)
+    return {k: (sorted(v[0]), sorted(v[1])) for k, v in sorted(groups.items())}
+
+
+def staging_bytes(old: Topology, new: Topology, L: int, H: int, D: int, elem_bytes: int,
+                  total_tokens: int) -> Dict[Tuple[int, int], int]:
+    """Byte size of every (r, q) staging buffer: all its slices, K and V."""
+    out = {}
+    for (r, q), (ls, hs) in pair_slices(old, new, L, H).items():
+        out[(r, q)] = 2 * total_tokens * len(ls) * len(hs) * D * elem_bytes
+    return out
+
+
+# ---------------------------------------------------------------------------
+# paging (where token t of sequence s lives)
+# ---------------------------------------------------------------------------
+
+def token_slots(tables, s: int) -> Tuple[np.ndarray, np.ndarray]:
+    """(block id, slot) of every live token of sequence s."""
+    n = int(tables.seq_lens[s])
+    t = np.arange(n, dtype=np.int64)
+    bs = int(tables.block_size)
+    row = np.asarray(tables.row(s), dtype=np.int64)
+    return row[t // bs], t % bs
+
+
+def token_offsets(seq_lens: np.ndarray) -> np.ndarray:
+    """Position of each sequence's first token in the sequence-major token axis."""
+    off = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+    off[1:] = np.cumsum(np.asarray(seq_lens, dtype=np.int64))
+    return off
+
+
+# ---------------------------------------------------------------------------
+# materialise and re-shard
+# ---------------------------------------------------------------------------
+
+def materialise(old_pools, old: Topology, L: int, H: int, old_tables, s: int, l: int,
+                heads: Iterable[int]) -> np.ndarray:
+    """Logical slice X[kv, t, h, :] of sequence s at layer l from the old shards.
+
+    Heads not in `heads` are left zero (their old owner need not be present).
+    """
+    heads = sorted(set(heads))
+    blk, slot = token_slots(old_tables, s)
+    n = blk.shape[0]
+    D, dtype = None, None
+    X = None
+    for h in heads:
+        r = owner(l, h, old, L, H)
+        store = old_pools[r][l]                          # [2, nb, bs, H_loc, D]
+        if X is None:
+            D, dtype = store.shape[-1], store.dtype
+            X = np.zeros((2, n, H, D), dtype=dtype)
+        h_loc = h - heads_of(r, old, H).start
+        X[:, :, h, :] = store[:, blk, slot, h_loc, :]
+    if X is None:
+        raise ValueError("no heads requested")
+    return X
+
+
+def reshard(old_pools, new_pools, old: Topology, new: Topology, L: int, H: int,
+            old_tables, new_tables, layers: Optional[Iterable[int]] = None,
+            pairs: Optional[Iterable[Tuple[int, int]]] = None):
+    """Re-shard the live KV cache from `old` to `new`.
+
+    old_pools: {old rank: {layer: [2, nb_o, bs_o, H/TP_o, D]}} -- read only.
+    new_pools: {new rank: {layer: [2, nb_n, bs_n, H/TP_n, D]}} -- written in
+               place at live slots only; ranks or layers absent are skipped.
+    layers:    global layers to process (default: all).
+    pairs:     (old rank, new rank) pairs whose staging to return (default: none).
+
+    Returns {(r, q): {layer: ndarray [2, T, |H_r & H_q|, D]}} for the requested
+    pairs and processed layers.
+    """
+    check_divisible(old, L, H)
+    check_divisible(new, L, H)
+    layers = range(L) if layers is None else sorted(set(layers))
+    pairs = [] if pairs is None else sorted(set(pairs))
+    S = len(old_tables.seq_lens)
+    if list(map(int, old_tables.seq_lens)) != list(map(int, new_tables.seq_lens)):
+        raise ValueError("old and new tables must describe the same sequences")
+    tok_off = token_offsets(old_tables.seq_lens)
+    T = int(tok_off[-1])
+    staging: Dict[Tuple[int, int], Dict[int, np.ndarray]] = {p: {} for p in pairs}
+
+    any_store = next(iter(next(iter(old_pools.values())).values()))
+    D, dtype = any_store.shape[-1], any_store.dtype
+    for l in layers:
+        # heads this layer must supply: to present new ranks, and to requested staging
+        need = set()
+        targets = []
+        for q, per_layer in new_pools.items():
+            if l in per_layer and l in layers_of(q, new, L):
+                targets.append(q)
+                need.update(heads_of(q, new, H))
+        slices = []
+        for (r, q) in pairs:
+            if l in layers_of(r, old, L) and l in layers_of(q, new, L):
+                hs = sorted(set(heads_of(r, old, H)) & set(heads_of(q, new, H)))
+                if hs:
+                    staging[(r, q)][l] = np.zeros((2, T, len(hs), D), dtype=dtype)
+                    slices.append(((r, q), hs))
+                    need.update(hs)
+        if not need:
+            continue
+        for s in range(S):
+            n = int(old_tables.seq_lens[s])
+            if n == 0:
+                continue
+            X = materialise(old_pools, old, L, H, old_tables, s, l, need)
+            nblk, nslot = token_slots(new_tables, s)
+            for q in targets:
+                hr = heads_of(q, new, H)
+                new_pools[q][l][:, nblk, nslot, :, :] = X[:, :, hr.start:hr.stop, :]
+            for key, hs in slices:
+                staging[key][l][:, tok_off[s]:tok_off[s] + n, :, :] = X[:, :, hs, :]
+    return staging
+
+
+def staging_buffer(items: Dict[int, np.ndarray]) -> np.ndarray:
+    """Concatenate a pair's slices in ascending layer order into one flat buffer."""
+    if not items:
+        return np.zeros(0, dtype=np.uint8)
+    parts = [np.ascontiguousarray(items[l]).reshape(-1).view(np.uint8) for l in sorted(items)]
+    return np.concatenate(parts)
+
+
+# ---------------------------------------------------------------------------
+# point queries (for checking sampled rows of very large migrations)
+# ---------------------------------------------------------------------------
+
+def old_location(l: int, h: int, s: int, t: int, old: Topology, L: int, H: int, old_tables):
+    """(old rank, block, slot, local head) holding token t of sequence s, layer l, head h."""
+    r = owner(l, h, old, L, H)
+    bs = int(old_tables.block_size)
+    blk = int(old_tables.row(s)[t // bs])
+    return r, blk, t % bs, h - heads_of(r, old, H).start
+
+
+def new_location(l: int, h: int, s: int, t: int, new: Topology, L: int, H: int, new_tables):
+    """(new rank, block, slot, local head) that must hold the same element after the switch."""
+    q = owner(l, h, new, L, H)
+    bs = int(new_tables.block_size)
+    blk = int(new_tables.row(s)[t // bs])
+    return q, blk, t % bs, h - heads_of(q, new, H).start
+
+
+def staging_location(r: int, q: int, l: int, kv: int, h: int, s: int, t: int, old: Topology,
+                     new: Topology, L: int, H: int, D: int, elem_bytes: int, seq_lens) -> int:
+    """Byte offset, in the (r, q) staging buffer, of row (l, kv, s, t, h)."""
+    ps = pair_slices(old, new, L, H)
+    ls, hs = ps[(r, q)]
+    if l not in ls or h not in hs:
+        raise ValueError("row is not part of this pair's staging")
+    tok_off = token_offsets(seq_lens)
+    T = int(tok_off[-1])
+    slice_bytes = 2 * T * len(hs) * D * elem_bytes
+    row = (kv * T + int(tok_off[s]) + t) * len(hs) + hs.index(h)
+    return ls.index(l) * slice_bytes + row * D * elem_bytes

@@ -1,0 +1,13 @@
+"""Seeded synthetic inputs for KV-cache migration (shared by the oracle's tests,
+the GPU tests and the benchmark; holds no migration arithmetic)."""
+from .configs import KVWorkload, WORKLOADS, TINY, MHA_7B, MHA_13B, GQA_70B, GQA_70B_LONG, reduced
+from .gen import (BlockTables, Inputs, make_inputs, make_tables, seq_lens, tables_from_rows,
+                  fill_words_, fill_pool_layer_, fill_sentinel_, words_at, bytes_at, stream_key,
+                  torch_dtype_for, numpy_dtype_for, SOURCE, SENTINEL)
+
+__all__ = [
+    "KVWorkload", "WORKLOADS", "TINY", "MHA_7B", "MHA_13B", "GQA_70B", "GQA_70B_LONG", "reduced",
+    "BlockTables", "Inputs", "make_inputs", "make_tables", "seq_lens", "tables_from_rows",
+    "fill_words_", "fill_pool_layer_", "fill_sentinel_", "words_at", "bytes_at", "stream_key",
+    "torch_dtype_for", "numpy_dtype_for", "SOURCE", "SENTINEL",
+]

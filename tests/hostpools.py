@@ -1,0 +1,61 @@
+"""Host-side (NumPy) pools filled from the shared seeded generator.
+
+Test harness code: builds the {rank: {layer: [2, nb, bs, H_loc, D]}} arrays the
+oracle reads and writes, with the same bytes the GPU tests put in HBM.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import synthkv
+
+
+def local_heads(H: int, tp: int) -> int:
+    return H // tp
+
+
+def rank_layers(r: int, tp: int, pp: int, L: int):
+    per = L // pp
+    p = r // tp
+    return range(p * per, (p + 1) * per)
+
+
+def source_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None):
+    """Old-pool contents for the given old ranks (default: all) and layers."""
+    tp, pp = w.old_topo
+    H_loc = local_heads(w.num_kv_heads, tp)
+    dt = synthkv.torch_dtype_for(w.elem_bytes)
+    out = {}
+    for r in (range(tp * pp) if ranks is None else ranks):
+        out[r] = {}
+        for l in rank_layers(r, tp, pp, w.num_layers):
+            if layers is not None and l not in layers:
+                continue
+            t = torch.empty((2, tables.num_blocks, tables.block_size, H_loc, w.head_dim), dtype=dt)
+            for kv in range(2):
+                synthkv.fill_pool_layer_(t[kv], w.seed, r, l, kv)
+            out[r][l] = t.numpy().view(synthkv.numpy_dtype_for(w.elem_bytes))
+    return out
+
+
+def sentinel_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None, tag: int = 0):
+    """New-pool pre-fill (sentinel stream) for the given new ranks."""
+    tp, pp = w.new_topo
+    H_loc = local_heads(w.num_kv_heads, tp)
+    dt = synthkv.torch_dtype_for(w.elem_bytes)
+    out = {}
+    for q in (range(tp * pp) if ranks is None else ranks):
+        out[q] = {}
+        for l in rank_layers(q, tp, pp, w.num_layers):
+            if layers is not None and l not in layers:
+                continue
+            t = torch.empty((2, tables.num_blocks, tables.block_size, H_loc, w.head_dim), dtype=dt)
+            for kv in range(2):
+                synthkv.fill_sentinel_(t[kv], w.seed, tag, q, l, kv)
+            out[q][l] = t.numpy().view(synthkv.numpy_dtype_for(w.elem_bytes))
+    return out
+
+
+def copy_pools(pools):
+    return {r: {l: a.copy() for l, a in d.items()} for r, d in pools.items()}

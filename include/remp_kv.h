@@ -1,0 +1,235 @@
+/*
+ * remp_kv.h -- two-dimensional KV-cache migration for MI355X (gfx950).
+ *
+ * When a serving instance changes its tensor-parallel (TP) or pipeline-parallel
+ * (PP) degree, every live K/V element keeps its identity but changes owner:
+ * element KV[l, b, h] held by rank(l, h, T_old) must end up on rank(l, h, T_new)
+ * (ReMP, Section 3.4.1).  TP changes re-slice the KV-head axis, PP changes
+ * re-assign the layer axis.  This library
+ *
+ *   1. builds the migration plan on the host: which (old rank, new rank) pairs
+ *      exchange which (layer, head-range) slices (Section 3.4.2, Algorithm 1);
+ *   2. packs, on the GPU, an old rank's live paged K/V rows into one contiguous
+ *      staging buffer per destination rank;
+ *   3. unpacks, on the GPU, the staging buffers a new rank receives into its
+ *      paged pool under the new block tables (the deterministic block remapping
+ *      of Section 3.4.5; the block size may change).
+ *
+ * The transfer of staging buffers between GPUs (Section 3.4.3) is the
+ * caller's: on one GPU the buffers simply stay in that GPU's memory.
+ *
+ * Conventions (readings of points the paper leaves open):
+ *   - ranks:  rank(pp, tp) = pp * TP + tp;
+ *   - layers: stage p of PP holds layers [p*L/PP, (p+1)*L/PP);  L % PP == 0;
+ *   - heads:  tensor rank t of TP holds KV heads [t*H/TP, (t+1)*H/TP); H % TP == 0;
+ *   - paged storage, per local layer, K and V separately:
+ *       [num_blocks][block_size][H/TP][head_dim] elements of elem_bytes bytes,
+ *     row-major; token t of sequence s lives in block ids[row_offsets[s] + t / block_size],
+ *     slot t % block_size; only tokens t < seq_lens[s] are live;
+ *   - staging of a pair (old rank r, new rank q): the pair's slices in ascending
+ *     layer order; one slice is
+ *       [kv: K then V][token: all sequences in order, live tokens only][head of the overlap][head_dim]
+ *     so a slice is 2 * T * head_count * head_dim * elem_bytes bytes, T = sum of seq_lens,
+ *     and any layer window is one contiguous byte range of the buffer.
+ *
+ * Elements are copied as raw bytes: any 1-, 2- or 4-byte type (fp8, fp16, bf16,
+ * fp32 ...) moves bit for bit, NaN payloads and signed zeros included.
+ *
+ * Threading: plan objects are immutable after creation and may be shared by
+ * threads.  The last-error text is per thread.  Pack and unpack are
+ * stream-ordered and asynchronous; a workspace must not be used by two calls
+ * that can run concurrently (different streams).  A plan must outlive the
+ * stream work its calls enqueued only for as long as the call itself runs:
+ * everything the kernels need is passed by value at launch.
+ */
+#ifndef REMP_KV_H
+#define REMP_KV_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REMP_API __attribute__((visibility("default")))
+
+typedef enum {
+    REMP_OK = 0,
+    REMP_E_INVALID = -1,     /* malformed argument: null pointer, inconsistent tables, duplicate block id */
+    REMP_E_UNSUPPORTED = -2, /* valid request this version does not handle: H % TP != 0, L % PP != 0 */
+    REMP_E_RANGE = -3,       /* rank, layer window or block id out of range */
+    REMP_E_CAPACITY = -4,    /* the new pool cannot hold the live cache (Section 3.4.5, capacity) */
+    REMP_E_ALIGN = -5,       /* a device pointer is not aligned to the element size */
+    REMP_E_SIZE = -6,        /* a workspace or staging buffer is smaller than required */
+    REMP_E_HIP = -7          /* a HIP runtime call or kernel launch failed */
+} remp_status;
+
+/* A parallel topology T = (TP, PP) (Section 3.4.1). */
+typedef struct {
+    int32_t tp;
+    int32_t pp;
+} remp_topo;
+
+/* Model KV shape.  elem_bytes in {1, 2, 4}.  The block size may differ between
+ * the old and the new pool. */
+typedef struct {
+    int32_t num_layers;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t elem_bytes;
+    int32_t old_block_size;
+    int32_t new_block_size;
+} remp_kv_shape;
+
+/* Block tables in host memory, CSR form: the row of sequence s is
+ * block_ids[row_offsets[s] .. row_offsets[s+1]); only its first
+ * ceil(seq_lens[s] / block_size) entries are read (the rest may be padding).
+ * num_blocks is the capacity of the pool the ids index. */
+typedef struct {
+    int32_t num_seqs;
+    const int32_t* seq_lens;     /* [num_seqs], >= 0 */
+    const int32_t* row_offsets;  /* [num_seqs + 1], non-decreasing, row_offsets[0] >= 0 */
+    const int32_t* block_ids;    /* [row_offsets[num_seqs]] */
+    int64_t num_blocks;
+} remp_block_tables;
+
+/* The same three arrays in device memory (the GPU copy a serving engine keeps
+ * for its attention kernels).  The contents must equal the host tables given
+ * for the same role; the kernels bound every access by the host sizes, so a
+ * mismatch cannot make them read or write outside the buffers, and it is
+ * reported through the workspace flag (see remp_kv_workspace_bytes). */
+typedef struct {
+    const int32_t* seq_lens;
+    const int32_t* row_offsets;
+    const int32_t* block_ids;
+} remp_dev_tables;
+
+/* A rank's paged KV storage: one K and one V device pointer per local layer
+ * (local layer i = global layer first_layer_of_rank + i), each addressing
+ * [num_blocks][block_size][H/TP][head_dim] elements.  Pointer arrays are host
+ * memory; entries for layers outside the call's layer window may be NULL. */
+typedef struct {
+    int32_t num_layers;
+    void* const* k;
+    void* const* v;
+    int64_t num_blocks;
+} remp_kv_pool;
+
+/* A device buffer and its size in bytes. */
+typedef struct {
+    void* ptr;
+    int64_t bytes;
+} remp_buffer;
+
+/* Sizes of a plan. */
+typedef struct {
+    int32_t old_world;        /* TP_old * PP_old */
+    int32_t new_world;        /* TP_new * PP_new */
+    int32_t num_pairs;        /* (old rank, new rank) pairs that exchange data */
+    int32_t num_items;        /* (old rank, new rank, layer) slices = Algorithm 1's send items */
+    int64_t total_tokens;     /* T = sum of seq_lens */
+    int64_t old_live_blocks;  /* sum of ceil(seq_lens / old_block_size) */
+    int64_t new_live_blocks;  /* sum of ceil(seq_lens / new_block_size) */
+} remp_kv_plan_info;
+
+/* One pair: old rank src sends new rank dst the heads
+ * [head_begin, head_begin + head_count) of layers [layer_begin, layer_end). */
+typedef struct {
+    int32_t src;
+    int32_t dst;
+    int32_t layer_begin;
+    int32_t layer_end;
+    int32_t head_begin;
+    int32_t head_count;
+    int64_t slice_bytes;      /* bytes of one layer's slice, K and V */
+    int64_t staging_bytes;    /* (layer_end - layer_begin) * slice_bytes */
+} remp_kv_pair;
+
+typedef struct remp_kv_plan_s remp_kv_plan_t;
+
+/* Build the migration plan for T_old -> T_new (Section 3.4.2, Algorithm 1:
+ * for every layer, intersect each new tensor rank's head range with each old
+ * tensor rank's; every non-empty overlap is one send item of the old rank and
+ * one receive item of the new rank, over all live blocks B).
+ * Copies what it needs from old_tables; the caller may free them afterwards.
+ * Validates shape (positive sizes, elem_bytes in {1,2,4}), divisibility
+ * (REMP_E_UNSUPPORTED), table structure (REMP_E_INVALID) and old block ids in
+ * [0, old_tables->num_blocks) (REMP_E_RANGE).  On failure *out is NULL. */
+REMP_API remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo,
+                         const remp_kv_shape* shape, const remp_block_tables* old_tables,
+                         remp_kv_plan_t** out);
+
+/* Free a plan; NULL is a no-op. */
+REMP_API void remp_kv_plan_destroy(remp_kv_plan_t* plan);
+
+REMP_API remp_status remp_kv_plan_get_info(const remp_kv_plan_t* plan, remp_kv_plan_info* out);
+
+/* The i-th pair, pairs ordered by (src, dst); 0 <= index < num_pairs. */
+REMP_API remp_status remp_kv_plan_get_pair(const remp_kv_plan_t* plan, int32_t index, remp_kv_pair* out);
+
+/* Staging size of pair (src, dst) (0 if the pair exchanges nothing) and, if
+ * layer_offsets is not NULL, its num_layers + 1 layer offsets: layer_offsets[l]
+ * is the byte offset of the first slice of a layer >= l, so a window [l0, l1)
+ * occupies bytes [layer_offsets[l0], layer_offsets[l1]). */
+REMP_API remp_status remp_kv_plan_query(const remp_kv_plan_t* plan, int32_t src, int32_t dst,
+                               int64_t* staging_bytes, int64_t* layer_offsets);
+
+/* Workspace bytes needed by remp_kv_pack and remp_kv_unpack with this plan.
+ * The workspace is device memory, 256-byte aligned, owned by the caller.
+ * After the stream work of a call completes, its first 4 bytes hold 0 if the
+ * device tables agreed with the host tables and a non-zero flag otherwise. */
+REMP_API remp_status remp_kv_workspace_bytes(const remp_kv_plan_t* plan, int64_t* bytes);
+
+/* Pack (Section 3.4.2 send side, Section 3.4.3): for every slice old_rank sends
+ * whose layer lies in [layer_begin, layer_end), copy its live rows from src
+ * into the destination's staging buffer.  staging has new_world entries, by
+ * destination rank; staging[q].ptr addresses the window's part of the (old_rank,
+ * q) buffer, i.e. byte layer_offsets[layer_begin] of the whole buffer, and
+ * staging[q].bytes must cover the window's slices.  Entries of ranks that get
+ * nothing in the window may be {NULL, 0}.  Never writes src (the source
+ * topology stays intact until the caller commits, Section 3.7).
+ * old_tables: device copy of the tables given to remp_kv_plan.
+ * Everything is validated before anything is enqueued; on error nothing is. */
+REMP_API remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank,
+                         int32_t layer_begin, int32_t layer_end,
+                         const remp_kv_pool* src, const remp_dev_tables* old_tables,
+                         const remp_buffer* staging,
+                         void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* Unpack (Section 3.4.2 receive side, Section 3.4.4 per layer window): for
+ * every slice new_rank receives whose layer lies in [layer_begin, layer_end),
+ * copy it from the source's staging buffer into dst at the live slots given by
+ * new_tables.  staging has old_world entries, by source rank, addressed like
+ * remp_kv_pack's.  Writes exactly the live (layer, token, head) rows of
+ * new_rank's shard and nothing else.
+ * new_tables (host) is validated: same sequences and lengths as the plan, rows
+ * long enough, ids in [0, new_tables->num_blocks), no id used twice
+ * (REMP_E_INVALID), enough blocks for the live cache (REMP_E_CAPACITY), and
+ * dst->num_blocks >= new_tables->num_blocks (REMP_E_SIZE).
+ * new_dev_tables: device copy of new_tables. */
+REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank,
+                           int32_t layer_begin, int32_t layer_end,
+                           const remp_buffer* staging,
+                           const remp_kv_pool* dst, const remp_block_tables* new_tables,
+                           const remp_dev_tables* new_dev_tables,
+                           void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* Measurement hook: while set (non-NULL), the calling thread's pack and unpack
+ * calls record `start` immediately before and `stop` immediately after their
+ * copy kernel(s) on the call's stream.  Pass NULL, NULL to clear. */
+REMP_API void remp_kv_set_trace_events(hipEvent_t start, hipEvent_t stop);
+
+REMP_API const char* remp_status_string(remp_status status);
+
+/* Detail of the calling thread's last failure ("" if none). */
+REMP_API const char* remp_last_error(void);
+
+/* Library version, e.g. "0.1.0". */
+REMP_API const char* remp_kv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REMP_KV_H */

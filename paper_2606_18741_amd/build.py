@@ -1,0 +1,64 @@
+"""Build libremp_kv.so for gfx950 in-tree with hipcc.
+
+    python paper_2606_18741_amd/build.py      (a plain script: importing the package needs the library)
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG, "libremp_kv.so")
+
+SOURCES = [os.path.join(CSRC, "plan.cpp"), os.path.join(CSRC, "migrate.hip")]
+
+HIPCC_FLAGS = [
+    "--offload-arch=gfx950",
+    "-O3",
+    "-std=c++17",
+    "-fPIC",
+    "-shared",
+    "-Wall",
+    "-fvisibility=hidden",
+    # never emit packed fp32 instructions (the library has no float math; this keeps it so)
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", INCLUDE,
+    "-I", CSRC,
+]
+
+# the host-only planner is plain C++; it sees the HIP headers only for hipStream_t / hipEvent_t
+CXX_FLAGS = ["-D__HIP_PLATFORM_AMD__"]
+
+
+def hipcc() -> str:
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    return os.path.join(rocm, "bin", "hipcc")
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source into LIB (always recompiles).  Returns the library path."""
+    tmp = LIB + ".tmp"
+    rocm_inc = os.path.join(os.path.dirname(os.path.dirname(hipcc())), "include")
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", rocm_inc, "-o", tmp]
+    for src in SOURCES:
+        if src.endswith(".hip"):
+            cmd += ["-x", "hip", src]
+        else:
+            cmd += [*CXX_FLAGS, "-x", "c++", src]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{res.stdout}\n{res.stderr}")
+    if verbose and res.stderr.strip():
+        print(res.stderr, file=sys.stderr)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,574 @@
+// GPU side of the KV-cache migration for gfx950: block-table expansion and the
+// pack / unpack copy kernels, plus the two C entry points that launch them.
+//
+// The copy is pure data movement (no arithmetic on the payload), so it is
+// bound by HBM bandwidth.  The layout makes every 16-byte vector of a slice
+// have exactly one source and one destination:
+//   paged side   [block][slot][local head][head_dim]  (a row run of head_count*head_dim
+//                elements at a stride of H_loc*head_dim)
+//   staging side [kv][token][head of the overlap][head_dim] (contiguous per block)
+// so both directions are coalesced row copies.  A workgroup owns a chunk of
+// consecutive block descriptors of one slice; its lanes stride over the
+// chunk's flattened (descriptor, kv, slot, vector) space with several 16-byte
+// loads in flight before their stores.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "plan.hpp"
+
+namespace remp {
+
+// ---------------------------------------------------------------------------
+// device data structures
+// ---------------------------------------------------------------------------
+
+// One live block of one sequence: physical block id, position of its first
+// token on the sequence-major token axis, number of live tokens in it.
+struct BlockDesc {
+    int32_t block;
+    int32_t tok;
+    int32_t n;
+    int32_t pad;
+};
+
+// Division by a runtime constant d for any 32-bit numerator (Granlund and
+// Montgomery, "Division by invariant integers using multiplication", 1994):
+// with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+// n / d = (mulhi(m, n) + n) >> l, the sum taken in 33 bits.
+struct FastDiv {
+    uint32_t magic;
+    uint32_t shift;
+};
+
+static FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while ((uint64_t(1) << l) < d) ++l;
+    uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1;
+    return FastDiv{static_cast<uint32_t>(m), l};
+}
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t magic, uint32_t shift) {
+    uint64_t t = __umulhi(n, magic);
+    return static_cast<uint32_t>((t + n) >> shift);
+}
+
+constexpr int kMaxItems = 64;         // slices per copy launch (kernel arguments stay < 4 KiB)
+constexpr int kMaxDescPerWg = 64;     // block descriptors per workgroup
+constexpr int kCopyThreads = 256;
+constexpr int kScanThreads = 1024;
+
+struct CopyItem {
+    uint64_t paged_k;     // K storage of the layer, offset to the slice's first head
+    uint64_t paged_v;
+    uint64_t stage;       // first byte of the slice in its staging buffer (K part)
+    uint32_t row_bytes;   // head_count * head_dim * elem_bytes
+    uint32_t vpr_magic;   // fast division by vectors per row
+    uint32_t unit_magic;  // fast division by vectors per (block, kv) unit
+    uint16_t vpr_shift;
+    uint16_t unit_shift;
+};
+
+struct CopyArgs {
+    const BlockDesc* desc;
+    int64_t block_stride;     // bytes per block on the paged side
+    int64_t total_tokens;     // T: a slice's V part starts T * row_bytes after its K part
+    int32_t n_desc;
+    int32_t descs_per_wg;
+    int32_t row_stride;       // bytes per token row on the paged side (all local heads)
+    int32_t block_size;       // paged-side block size
+    CopyItem items[kMaxItems];
+};
+
+// ---------------------------------------------------------------------------
+// expansion: block tables -> one descriptor per live block
+// ---------------------------------------------------------------------------
+
+// Exclusive prefix sums of tokens and of blocks per sequence (one workgroup,
+// wave64 shuffle scans combined through LDS, carried across chunks of 1024).
+__global__ __launch_bounds__(kScanThreads) void expand_scan(const int32_t* __restrict__ lens, int32_t S,
+                                                           int32_t bs, int32_t* __restrict__ flag,
+                                                           int32_t* __restrict__ tok_off,
+                                                           int32_t* __restrict__ blk_off) {
+    __shared__ int64_t wave_tok[kScanThreads / 64];
+    __shared__ int64_t wave_blk[kScanThreads / 64];
+    __shared__ int64_t carry[2];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) {
+        carry[0] = 0;
+        carry[1] = 0;
+        *flag = 0;
+    }
+    __syncthreads();
+    bool bad = false;
+    for (int32_t base = 0; base < S; base += kScanThreads) {
+        const int32_t s = base + tid;
+        int64_t n = s < S ? lens[s] : 0;
+        if (n < 0) {
+            n = 0;
+            bad = true;
+        }
+        const int64_t nb = (n + bs - 1) / bs;
+        int64_t it = n, ib = nb;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int64_t a = __shfl_up(it, d, 64);
+            const int64_t b = __shfl_up(ib, d, 64);
+            if (lane >= d) {
+                it += a;
+                ib += b;
+            }
+        }
+        if (lane == 63) {
+            wave_tok[wave] = it;
+            wave_blk[wave] = ib;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            const int nw = kScanThreads / 64;
+            int64_t wt = lane < nw ? wave_tok[lane] : 0;
+            int64_t wb = lane < nw ? wave_blk[lane] : 0;
+#pragma unroll
+            for (int d = 1; d < nw; d <<= 1) {
+                const int64_t a = __shfl_up(wt, d, 64);
+                const int64_t b = __shfl_up(wb, d, 64);
+                if (lane >= d) {
+                    wt += a;
+                    wb += b;
+                }
+            }
+            if (lane < nw) {   // exclusive totals of preceding waves
+                wave_tok[lane] = wt;
+                wave_blk[lane] = wb;
+            }
+        }
+        __syncthreads();
+        const int64_t pre_t = carry[0] + (wave ? wave_tok[wave - 1] : 0);
+        const int64_t pre_b = carry[1] + (wave ? wave_blk[wave - 1] : 0);
+        if (s < S) {
+            const int64_t et = pre_t + it - n, eb = pre_b + ib - nb;
+            if (et > INT32_MAX || eb > INT32_MAX) bad = true;
+            tok_off[s] = static_cast<int32_t>(et < INT32_MAX ? et : INT32_MAX);
+            blk_off[s] = static_cast<int32_t>(eb < INT32_MAX ? eb : INT32_MAX);
+        }
+        __syncthreads();
+        if (tid == kScanThreads - 1) {
+            carry[0] = pre_t + it;
+            carry[1] = pre_b + ib;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        tok_off[S] = static_cast<int32_t>(carry[0] < INT32_MAX ? carry[0] : INT32_MAX);
+        blk_off[S] = static_cast<int32_t>(carry[1] < INT32_MAX ? carry[1] : INT32_MAX);
+    }
+    if (bad) *flag = 1;
+}
+
+// One thread per live block: locate its sequence by binary search over the
+// block offsets, then read its id from the table row.  Every index is bounded
+// by the host-side sizes; an inconsistency yields an empty descriptor and sets
+// the flag instead of an out-of-bounds access.
+__global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ lens,
+                                                   const int32_t* __restrict__ row_off,
+                                                   const int32_t* __restrict__ ids, int32_t S, int32_t bs,
+                                                   const int32_t* __restrict__ tok_off,
+                                                   const int32_t* __restrict__ blk_off, int64_t nnz,
+                                                   int64_t num_blocks, int64_t total_tokens, int64_t n_desc,
+                                                   BlockDesc* __restrict__ desc, int32_t* __restrict__ flag) {
+    const int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (b >= n_desc) return;
+    int32_t lo = 0, hi = S;   // last s in [0, S] with blk_off[s] <= b
+    while (lo < hi) {
+        const int32_t mid = (lo + hi + 1) >> 1;
+        if (blk_off[mid] <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    BlockDesc d{0, 0, 0, 0};
+    bool ok = lo < S;
+    if (ok) {
+        const int32_t s = lo;
+        const int64_t j = b - blk_off[s];
+        const int64_t n = lens[s];
+        const int64_t r = static_cast<int64_t>(row_off[s]) + j;
+        ok = r >= 0 && r < nnz;
+        if (ok) {
+            const int64_t id = ids[r];
+            const int64_t tok = static_cast<int64_t>(tok_off[s]) + j * bs;
+            const int64_t rest = n - j * bs;
+            const int64_t cnt = rest < bs ? rest : bs;
+            ok = id >= 0 && id < num_blocks && cnt > 0 && tok >= 0 && tok + cnt <= total_tokens;
+            if (ok) d = BlockDesc{static_cast<int32_t>(id), static_cast<int32_t>(tok), static_cast<int32_t>(cnt), 0};
+        }
+    }
+    if (!ok) *flag = 1;
+    desc[b] = d;
+}
+
+// ---------------------------------------------------------------------------
+// pack / unpack copy
+// ---------------------------------------------------------------------------
+
+template <int VEC> struct VecT;
+template <> struct VecT<16> { typedef unsigned int type __attribute__((ext_vector_type(4))); };
+template <> struct VecT<8> { typedef unsigned int type __attribute__((ext_vector_type(2))); };
+template <> struct VecT<4> { typedef unsigned int type; };
+template <> struct VecT<2> { typedef unsigned short type; };
+template <> struct VecT<1> { typedef unsigned char type; };
+
+template <int VEC, bool PACK, int UNROLL>
+__global__ __launch_bounds__(kCopyThreads) void copy_slices(const CopyArgs args) {
+    typedef typename VecT<VEC>::type V;
+    __shared__ uint64_t s_paged[2 * kMaxDescPerWg];
+    __shared__ uint64_t s_stage[2 * kMaxDescPerWg];
+    __shared__ int32_t s_n[2 * kMaxDescPerWg];
+
+    const CopyItem& it = args.items[blockIdx.y];
+    const int32_t d0 = static_cast<int32_t>(blockIdx.x) * args.descs_per_wg;
+    const int32_t nd = min(args.descs_per_wg, args.n_desc - d0);
+    const int tid = threadIdx.x;
+    const uint64_t kv_stride = static_cast<uint64_t>(args.total_tokens) * it.row_bytes;
+
+    // unit u = (descriptor d0 + u/2, kv = u%2): base addresses of its two sides
+    for (int u = tid; u < 2 * nd; u += kCopyThreads) {
+        const BlockDesc d = args.desc[d0 + (u >> 1)];
+        const int kv = u & 1;
+        s_paged[u] = (kv ? it.paged_v : it.paged_k) + static_cast<uint64_t>(d.block) * args.block_stride;
+        s_stage[u] = it.stage + kv * kv_stride + static_cast<uint64_t>(d.tok) * it.row_bytes;
+        s_n[u] = d.n;
+    }
+    __syncthreads();
+
+    const uint32_t vpr = it.row_bytes / VEC;
+    const uint32_t unit = static_cast<uint32_t>(args.block_size) * vpr;
+    const uint32_t total = static_cast<uint32_t>(2 * nd) * unit;
+    const uint32_t row_stride = static_cast<uint32_t>(args.row_stride);
+
+    for (uint32_t base = tid; base < total; base += kCopyThreads * UNROLL) {
+        V r[UNROLL];
+        uint64_t dst[UNROLL];
+        bool ok[UNROLL];
+#pragma unroll
+        for (int j = 0; j < UNROLL; ++j) {
+            const uint32_t idx = base + j * kCopyThreads;
+            ok[j] = false;
+            dst[j] = 0;
+            if (idx < total) {
+                const uint32_t u = fast_div(idx, it.unit_magic, it.unit_shift);
+                const uint32_t rem = idx - u * unit;
+                const uint32_t row = fast_div(rem, it.vpr_magic, it.vpr_shift);
+                const uint32_t c = rem - row * vpr;
+                if (static_cast<int32_t>(row) < s_n[u]) {
+                    const uint64_t paged = s_paged[u] + static_cast<uint64_t>(row) * row_stride + c * VEC;
+                    const uint64_t stage = s_stage[u] + static_cast<uint64_t>(rem) * VEC;
+                    const uint64_t src = PACK ? paged : stage;
+                    dst[j] = PACK ? stage : paged;
+                    r[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(src));
+                    ok[j] = true;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < UNROLL; ++j)
+            if (ok[j]) __builtin_nontemporal_store(r[j], reinterpret_cast<V*>(dst[j]));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host launch code
+// ---------------------------------------------------------------------------
+
+static thread_local hipEvent_t g_trace_start = nullptr;
+static thread_local hipEvent_t g_trace_stop = nullptr;
+
+static int env_int(const char* name, int dflt) {
+    const char* v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    return std::atoi(v);
+}
+
+struct HostSlice {
+    uint64_t paged_k, paged_v, stage;
+    uint32_t row_bytes;
+};
+
+static remp_status hip_check(hipError_t e, const char* what) {
+    if (e == hipSuccess) return REMP_OK;
+    return fail(REMP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Enqueue expansion of `tables` into descriptors in the workspace.
+static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables& dt, int32_t bs, int64_t nnz,
+                                 int64_t num_blocks, int64_t n_desc, char* ws, hipStream_t stream) {
+    int32_t* flag = reinterpret_cast<int32_t*>(ws);
+    int32_t* tok_off = reinterpret_cast<int32_t*>(ws + 256);
+    int32_t* blk_off = tok_off + (p.num_seqs + 1);
+    BlockDesc* desc = reinterpret_cast<BlockDesc*>(ws + workspace_desc_offset(p));
+    hipLaunchKernelGGL(expand_scan, dim3(1), dim3(kScanThreads), 0, stream, dt.seq_lens, p.num_seqs, bs, flag,
+                       tok_off, blk_off);
+    if (remp_status st = hip_check(hipGetLastError(), "expand_scan launch")) return st;
+    if (n_desc > 0) {
+        const int64_t blocks = (n_desc + 255) / 256;
+        hipLaunchKernelGGL(expand_emit, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, dt.seq_lens,
+                           dt.row_offsets, dt.block_ids, p.num_seqs, bs, tok_off, blk_off, nnz, num_blocks,
+                           p.total_tokens, n_desc, desc, flag);
+        if (remp_status st = hip_check(hipGetLastError(), "expand_emit launch")) return st;
+    }
+    return REMP_OK;
+}
+
+template <int VEC, bool PACK>
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, hipStream_t stream) {
+    hipLaunchKernelGGL((copy_slices<VEC, PACK, 8>), grid, dim3(kCopyThreads), 0, stream, a);
+}
+
+template <bool PACK>
+static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSlice>& slices, int64_t n_desc,
+                               int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
+                               hipStream_t stream) {
+    if (slices.empty() || n_desc == 0) return REMP_OK;
+    // widest vector every address and stride is aligned to
+    uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(row_stride) | 16u;
+    uint32_t max_row = 0;
+    for (const HostSlice& s : slices) {
+        bits |= s.paged_k | s.paged_v | s.stage | s.row_bytes |
+                (static_cast<uint64_t>(p.total_tokens) * s.row_bytes);
+        max_row = std::max(max_row, s.row_bytes);
+    }
+    const int vec = static_cast<int>(bits & (~bits + 1));   // lowest set bit, <= 16
+    const int64_t target = env_int("REMP_KV_WG_BYTES", 64 * 1024);
+    const int64_t per_desc = 2 * static_cast<int64_t>(bs) * max_row;
+    int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxDescPerWg, target / per_desc)));
+    // the flattened per-workgroup index must stay below 2^32
+    while (C > 1 && static_cast<uint64_t>(2) * C * bs * (max_row / vec) >= (uint64_t(1) << 32)) C >>= 1;
+    if (static_cast<uint64_t>(2) * bs * (max_row / vec) >= (uint64_t(1) << 32))
+        return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^32 vectors");
+
+    CopyArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.desc = reinterpret_cast<const BlockDesc*>(ws + workspace_desc_offset(p));
+    a.block_stride = block_stride;
+    a.total_tokens = p.total_tokens;
+    a.n_desc = static_cast<int32_t>(n_desc);
+    a.descs_per_wg = C;
+    a.row_stride = row_stride;
+    a.block_size = bs;
+    const int64_t gx = (n_desc + C - 1) / C;
+    if (gx > 0x7FFFFFFF) return fail(REMP_E_UNSUPPORTED, "too many block descriptors for one launch");
+
+    if (g_trace_start) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
+    }
+    for (size_t first = 0; first < slices.size(); first += kMaxItems) {
+        const size_t cnt = std::min<size_t>(kMaxItems, slices.size() - first);
+        for (size_t i = 0; i < cnt; ++i) {
+            const HostSlice& s = slices[first + i];
+            CopyItem& c = a.items[i];
+            c.paged_k = s.paged_k;
+            c.paged_v = s.paged_v;
+            c.stage = s.stage;
+            c.row_bytes = s.row_bytes;
+            const FastDiv fv = make_fastdiv(s.row_bytes / vec);
+            const FastDiv fu = make_fastdiv(static_cast<uint32_t>(bs) * (s.row_bytes / vec));
+            c.vpr_magic = fv.magic;
+            c.vpr_shift = static_cast<uint16_t>(fv.shift);
+            c.unit_magic = fu.magic;
+            c.unit_shift = static_cast<uint16_t>(fu.shift);
+        }
+        const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
+        switch (vec) {
+            case 16: launch_copy_vec<16, PACK>(a, grid, stream); break;
+            case 8: launch_copy_vec<8, PACK>(a, grid, stream); break;
+            case 4: launch_copy_vec<4, PACK>(a, grid, stream); break;
+            case 2: launch_copy_vec<2, PACK>(a, grid, stream); break;
+            default: launch_copy_vec<1, PACK>(a, grid, stream); break;
+        }
+        if (remp_status st = hip_check(hipGetLastError(), PACK ? "pack launch" : "unpack launch")) return st;
+    }
+    if (g_trace_stop) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_stop, stream), "trace stop event")) return st;
+    }
+    return REMP_OK;
+}
+
+static bool aligned(const void* p, int64_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+static remp_status check_common(const remp_kv_plan_t* plan, int32_t l0, int32_t l1, const remp_kv_pool* pool,
+                                const remp_buffer* staging, void* ws, int64_t ws_bytes, int32_t layers_per_rank) {
+    if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (l0 < 0 || l1 < l0 || l1 > plan->shape.num_layers)
+        return fail(REMP_E_RANGE, "layer window [" + std::to_string(l0) + ", " + std::to_string(l1) +
+                                      ") outside [0, " + std::to_string(plan->shape.num_layers) + "]");
+    if (!pool) return fail(REMP_E_INVALID, "pool is NULL");
+    if (pool->num_layers != layers_per_rank)
+        return fail(REMP_E_INVALID, "pool has " + std::to_string(pool->num_layers) + " layers, the rank holds " +
+                                        std::to_string(layers_per_rank));
+    if (!pool->k || !pool->v) return fail(REMP_E_INVALID, "pool pointer arrays are NULL");
+    if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
+    if (!ws) return fail(REMP_E_INVALID, "workspace is NULL");
+    if (!aligned(ws, 256)) return fail(REMP_E_ALIGN, "workspace is not 256-byte aligned");
+    if (ws_bytes < workspace_bytes(*plan))
+        return fail(REMP_E_SIZE, "workspace has " + std::to_string(ws_bytes) + " bytes, needs " +
+                                     std::to_string(workspace_bytes(*plan)));
+    return REMP_OK;
+}
+
+// Slices of the window for one side; fills `out`.  `pack`: items of old rank
+// `rank`; else items of new rank `rank`.
+static remp_status collect_slices(const remp_kv_plan_t& p, bool pack, int32_t rank, int32_t l0, int32_t l1,
+                                  const remp_kv_pool& pool, const remp_buffer* staging,
+                                  std::vector<HostSlice>& out) {
+    const Ownership& mine = pack ? p.own_old : p.own_new;
+    const int64_t hrow = static_cast<int64_t>(p.shape.head_dim) * p.shape.elem_bytes;
+    const int32_t eb = p.shape.elem_bytes;
+    for (const Item& it : p.items) {
+        if ((pack ? it.src : it.dst) != rank || it.layer < l0 || it.layer >= l1) continue;
+        const Pair& pr = p.pairs[it.pair];
+        const int32_t peer = pack ? it.dst : it.src;
+        const int32_t ws0 = std::max(l0, pr.layer_begin), ws1 = std::min(l1, pr.layer_end);
+        const remp_buffer& sb = staging[peer];
+        const int64_t need = static_cast<int64_t>(ws1 - ws0) * pr.slice_bytes;
+        if (need > 0) {
+            if (!sb.ptr)
+                return fail(REMP_E_INVALID, std::string("staging buffer for ") + (pack ? "destination " : "source ") +
+                                                std::to_string(peer) + " is NULL");
+            if (sb.bytes < need)
+                return fail(REMP_E_SIZE, "staging buffer for rank " + std::to_string(peer) + " has " +
+                                             std::to_string(sb.bytes) + " bytes, the window needs " +
+                                             std::to_string(need));
+            if (!aligned(sb.ptr, eb)) return fail(REMP_E_ALIGN, "staging buffer not element aligned");
+        }
+        const int32_t li = it.layer - mine.first_layer(rank);
+        void* k = pool.k[li];
+        void* v = pool.v[li];
+        if (!k || !v)
+            return fail(REMP_E_INVALID, "pool storage of layer " + std::to_string(it.layer) + " is NULL");
+        if (!aligned(k, eb) || !aligned(v, eb)) return fail(REMP_E_ALIGN, "pool storage not element aligned");
+        const int64_t hoff = static_cast<int64_t>(it.head_begin - mine.first_head(rank)) * hrow;
+        HostSlice s;
+        s.paged_k = reinterpret_cast<uint64_t>(k) + hoff;
+        s.paged_v = reinterpret_cast<uint64_t>(v) + hoff;
+        s.stage = reinterpret_cast<uint64_t>(sb.ptr) + static_cast<uint64_t>(it.layer - ws0) * pr.slice_bytes;
+        s.row_bytes = static_cast<uint32_t>(it.head_count * hrow);
+        out.push_back(s);
+    }
+    return REMP_OK;
+}
+
+}  // namespace remp
+
+using namespace remp;
+
+extern "C" {
+
+void remp_kv_set_trace_events(hipEvent_t start, hipEvent_t stop) {
+    g_trace_start = start;
+    g_trace_stop = stop;
+}
+
+remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t layer_begin, int32_t layer_end,
+                         const remp_kv_pool* src, const remp_dev_tables* old_tables, const remp_buffer* staging,
+                         void* workspace, int64_t workspace_bytes_, hipStream_t stream) {
+    clear_error();
+    if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (old_rank < 0 || old_rank >= plan->own_old.world())
+        return fail(REMP_E_RANGE, "old_rank " + std::to_string(old_rank) + " outside [0, " +
+                                      std::to_string(plan->own_old.world()) + ")");
+    if (remp_status st = check_common(plan, layer_begin, layer_end, src, staging, workspace, workspace_bytes_,
+                                      plan->own_old.layers_per_stage()))
+        return st;
+    if (src->num_blocks < plan->old_num_blocks)
+        return fail(REMP_E_SIZE, "source pool has fewer blocks than the old tables address");
+    if (!old_tables) return fail(REMP_E_INVALID, "device old tables are NULL");
+    if (plan->num_seqs > 0 && (!old_tables->seq_lens || !old_tables->row_offsets))
+        return fail(REMP_E_INVALID, "device old table arrays are NULL");
+    if (plan->old_nnz > 0 && !old_tables->block_ids) return fail(REMP_E_INVALID, "device old block ids are NULL");
+
+    std::vector<HostSlice> slices;
+    if (remp_status st = collect_slices(*plan, true, old_rank, layer_begin, layer_end, *src, staging, slices))
+        return st;
+    if (slices.empty() || plan->old_live_blocks == 0) return REMP_OK;
+    const remp_kv_shape& sh = plan->shape;
+    const int64_t row_stride = static_cast<int64_t>(plan->own_old.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
+    char* ws = static_cast<char*>(workspace);
+    if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz, plan->old_num_blocks,
+                                       plan->old_live_blocks, ws, stream))
+        return st;
+    return launch_copy<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size, row_stride * sh.old_block_size,
+                             static_cast<int32_t>(row_stride), ws, stream);
+}
+
+remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t layer_begin, int32_t layer_end,
+                           const remp_buffer* staging, const remp_kv_pool* dst, const remp_block_tables* new_tables,
+                           const remp_dev_tables* new_dev_tables, void* workspace, int64_t workspace_bytes_,
+                           hipStream_t stream) {
+    clear_error();
+    if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (new_rank < 0 || new_rank >= plan->own_new.world())
+        return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
+                                      std::to_string(plan->own_new.world()) + ")");
+    if (remp_status st = check_common(plan, layer_begin, layer_end, dst, staging, workspace, workspace_bytes_,
+                                      plan->own_new.layers_per_stage()))
+        return st;
+    // --- new tables: same population, valid rows, ids in range and used once
+    if (!new_tables) return fail(REMP_E_INVALID, "new tables are NULL");
+    const remp_block_tables& t = *new_tables;
+    const remp_kv_shape& sh = plan->shape;
+    if (t.num_seqs != plan->num_seqs) return fail(REMP_E_INVALID, "new tables describe a different number of sequences");
+    if (t.num_seqs > 0 && (!t.seq_lens || !t.row_offsets)) return fail(REMP_E_INVALID, "new table arrays are NULL");
+    if (t.num_blocks < 0 || t.num_blocks > INT32_MAX) return fail(REMP_E_INVALID, "new num_blocks out of range");
+    if (plan->new_live_blocks > t.num_blocks)
+        return fail(REMP_E_CAPACITY, "the live cache needs " + std::to_string(plan->new_live_blocks) +
+                                         " blocks, the new pool has " + std::to_string(t.num_blocks));
+    if (dst->num_blocks < t.num_blocks) return fail(REMP_E_SIZE, "destination pool smaller than its tables");
+    int64_t nnz = 0;
+    if (t.num_seqs > 0) {
+        if (t.row_offsets[0] < 0) return fail(REMP_E_INVALID, "new row_offsets[0] < 0");
+        nnz = t.row_offsets[t.num_seqs];
+        if (nnz > 0 && !t.block_ids) return fail(REMP_E_INVALID, "new block_ids is NULL");
+    }
+    {
+        std::vector<uint8_t> used(static_cast<size_t>(t.num_blocks), 0);
+        for (int32_t q = 0; q < t.num_seqs; ++q) {
+            if (t.seq_lens[q] != plan->seq_lens[q])
+                return fail(REMP_E_INVALID, "new tables give sequence " + std::to_string(q) + " length " +
+                                                std::to_string(t.seq_lens[q]) + ", planned " +
+                                                std::to_string(plan->seq_lens[q]));
+            const int32_t a = t.row_offsets[q], b = t.row_offsets[q + 1];
+            if (b < a) return fail(REMP_E_INVALID, "new row_offsets decrease at sequence " + std::to_string(q));
+            const int64_t need = ceil_div(t.seq_lens[q], sh.new_block_size);
+            if (b - a < need) return fail(REMP_E_INVALID, "new table row of sequence " + std::to_string(q) + " too short");
+            for (int64_t j = 0; j < need; ++j) {
+                const int32_t id = t.block_ids[a + j];
+                if (id < 0 || id >= t.num_blocks)
+                    return fail(REMP_E_RANGE, "new block id " + std::to_string(id) + " outside [0, " +
+                                                  std::to_string(t.num_blocks) + ")");
+                if (used[id]) return fail(REMP_E_INVALID, "new block id " + std::to_string(id) + " used twice");
+                used[id] = 1;
+            }
+        }
+    }
+    if (!new_dev_tables) return fail(REMP_E_INVALID, "device new tables are NULL");
+    if (plan->num_seqs > 0 && (!new_dev_tables->seq_lens || !new_dev_tables->row_offsets))
+        return fail(REMP_E_INVALID, "device new table arrays are NULL");
+    if (nnz > 0 && !new_dev_tables->block_ids) return fail(REMP_E_INVALID, "device new block ids are NULL");
+
+    std::vector<HostSlice> slices;
+    if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging, slices))
+        return st;
+    if (slices.empty() || plan->new_live_blocks == 0) return REMP_OK;
+    const int64_t row_stride = static_cast<int64_t>(plan->own_new.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
+    char* ws = static_cast<char*>(workspace);
+    if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, t.num_blocks,
+                                       plan->new_live_blocks, ws, stream))
+        return st;
+    return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
+                              static_cast<int32_t>(row_stride), ws, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,71 @@
+// Internal plan representation shared by the host planner and the launch code.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "remp_kv.h"
+
+namespace remp {
+
+// One send/receive item of the plan: old rank `src` ships heads
+// [head_begin, head_begin + head_count) of layer `layer` to new rank `dst`.
+struct Item {
+    int32_t src, dst, layer, head_begin, head_count;
+    int32_t pair;        // index into Plan::pairs
+};
+
+struct Pair {
+    int32_t src, dst;
+    int32_t layer_begin, layer_end;
+    int32_t head_begin, head_count;
+    int64_t slice_bytes;
+};
+
+struct Ownership {
+    int32_t tp, pp, L, H;
+    int32_t layers_per_stage() const { return L / pp; }
+    int32_t heads_per_rank() const { return H / tp; }
+    int32_t pp_owner(int32_t l) const { return l / layers_per_stage(); }
+    int32_t tp_owner(int32_t h) const { return h / heads_per_rank(); }
+    int32_t rank(int32_t stage, int32_t t) const { return stage * tp + t; }
+    int32_t stage_of(int32_t r) const { return r / tp; }
+    int32_t tp_of(int32_t r) const { return r % tp; }
+    int32_t first_layer(int32_t r) const { return stage_of(r) * layers_per_stage(); }
+    int32_t first_head(int32_t r) const { return tp_of(r) * heads_per_rank(); }
+    int32_t world() const { return tp * pp; }
+};
+
+}  // namespace remp
+
+struct remp_kv_plan_s {
+    remp_topo old_topo, new_topo;
+    remp_kv_shape shape;
+    remp::Ownership own_old, own_new;
+    int32_t num_seqs = 0;
+    std::vector<int32_t> seq_lens;
+    std::vector<int32_t> old_row_offsets;
+    std::vector<int32_t> old_block_ids;
+    int64_t old_num_blocks = 0;
+    int64_t old_nnz = 0;
+    int64_t total_tokens = 0;
+    int64_t old_live_blocks = 0;
+    int64_t new_live_blocks = 0;
+    std::vector<remp::Item> items;     // Algorithm 1 order: layer, then new tensor rank, then old tensor rank
+    std::vector<remp::Pair> pairs;     // ordered by (src, dst)
+    std::vector<int32_t> pair_index;   // [old_world * new_world] -> pair or -1
+};
+
+namespace remp {
+
+// Thread-local error reporting shared by every entry point.
+remp_status fail(remp_status st, const std::string& msg);
+void clear_error();
+
+int64_t ceil_div(int64_t a, int64_t b);
+int64_t workspace_bytes(const remp_kv_plan_t& p);
+int64_t workspace_desc_offset(const remp_kv_plan_t& p);
+const Pair* find_pair(const remp_kv_plan_t& p, int32_t src, int32_t dst);
+
+}  // namespace remp

@@ -1,0 +1,244 @@
+"""GPU parity: libremp_kv.so's pack and unpack against the CPU oracle, bit for bit.
+
+Small and reduced workloads run every old rank's pack and every new rank's
+unpack on the one GPU and compare every staging byte and every byte of every
+new pool (live slots and untouched sentinels alike) with the oracle; the
+source pools must come back unchanged.  Two hand-derived examples are also
+checked against their hand-written expected values directly.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthkv
+from synthkv import tables_from_rows
+
+import hostpools
+from gpu_harness import (DeviceTables, RankPool, Workspace, log, rank_layers, shape_of, stream_handle,
+                         staging_for_pairs, window_args)
+
+pytestmark = pytest.mark.gpu
+
+T = oracle.Topology
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rk():
+    import paper_2606_18741_amd as rk
+    return rk
+
+
+def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None):
+    """Pack every old rank, unpack every new rank, per layer window.  Returns device state."""
+    rk = _rk()
+    L = w.num_layers
+    plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(old_tables))
+    dto, dtn = DeviceTables(old_tables), DeviceTables(new_tables)
+    W_old, W_new = plan.info.old_world, plan.info.new_world
+    src = {r: RankPool.from_host(old_host[r], rank_layers(r, w.old_topo, L), old_tables.num_blocks, r)
+           for r in range(W_old)}
+    dst = {q: RankPool.from_host(new_host[q], rank_layers(q, w.new_topo, L), new_tables.num_blocks, q)
+           for q in range(W_new)}
+    pairs = [(p.src, p.dst) for p in plan.pairs]
+    staging = staging_for_pairs(plan, w.seed, pairs)
+    ws = Workspace(plan)
+    stream = stream_handle()
+    flags = []
+    for (l0, l1) in (windows or [(0, L)]):
+        for r in range(W_old):
+            plan.pack(r, src[r].arg, dto.dev, window_args(plan, staging, r, W_new, True, l0, l1),
+                      ws.buf, ws.bytes, stream, l0, l1)
+        torch.cuda.synchronize()
+        flags.append(ws.flag())
+        for q in range(W_new):
+            plan.unpack(q, window_args(plan, staging, q, W_old, False, l0, l1), dst[q].arg, dtn.host, dtn.dev,
+                        ws.buf, ws.bytes, stream, l0, l1)
+        torch.cuda.synchronize()
+        flags.append(ws.flag())
+    return plan, src, dst, staging, flags
+
+
+def check_against_oracle(w, inp, windows=None, log_name=""):
+    L, H = w.num_layers, w.num_kv_heads
+    old_host = hostpools.source_pools(w, inp.old_tables)
+    new_host = hostpools.sentinel_pools(w, inp.new_tables)
+    log(f"[parity] {log_name or w.name}: T={int(inp.lens.sum())} windows={windows}")
+    plan, src, dst, staging, flags = migrate_all(w, inp.old_tables, inp.new_tables, old_host, new_host, windows)
+    pairs = [(p.src, p.dst) for p in plan.pairs]
+    st = oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables,
+                        inp.new_tables, pairs=pairs)
+    assert all(f == 0 for f in flags), flags
+    for p in pairs:
+        want = oracle.staging_buffer(st[p])
+        if want.size == 0:
+            assert p not in staging or staging[p].numel() == 0
+            continue
+        got = staging[p].cpu().numpy()
+        assert got.shape == want.shape, (p, got.shape, want.shape)
+        if not np.array_equal(got, want):
+            bad = np.nonzero(got != want)[0]
+            pytest.fail(f"staging {p}: {bad.size} bytes differ, first at {bad[0]}")
+    for q, pool in dst.items():
+        got = pool.host(w.elem_bytes)
+        for l, a in new_host[q].items():
+            if not np.array_equal(got[l], a):
+                bad = np.argwhere(got[l] != a)
+                pytest.fail(f"new rank {q} layer {l}: {len(bad)} elements differ, first at {bad[0].tolist()}")
+    for r, pool in src.items():           # pack never writes its source
+        got = pool.host(w.elem_bytes)
+        for l, a in old_host[r].items():
+            assert np.array_equal(got[l], a), f"source rank {r} layer {l} modified"
+
+
+# ---------------------------------------------------------------------------
+# hand-derived examples (expected values written by hand, not by the oracle)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["hand_tp2pp1_to_tp1pp2.json", "hand_tp1pp2_to_tp2pp1_reblock.json"])
+def test_golden_hand_example_gpu(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        g = json.load(f)
+    w = synthkv.KVWorkload(name="golden", num_layers=g["num_layers"], num_kv_heads=g["num_kv_heads"],
+                           head_dim=g["head_dim"], elem_bytes=2, dtype="u16", old_block_size=g["old_block_size"],
+                           new_block_size=g["new_block_size"], num_seqs=len(g["seq_lens"]),
+                           length_law=("fixed", 0), pool_law=("fixed", 0), old_topo=tuple(g["old_topo"]),
+                           new_topo=tuple(g["new_topo"]), role="all", seed=0)
+    old_t = tables_from_rows(g["seq_lens"], g["old_rows"], g["old_num_blocks"], g["old_block_size"])
+    new_t = tables_from_rows(g["seq_lens"], g["new_rows"], g["new_num_blocks"], g["new_block_size"])
+    old_host = {}
+    for key, arr in g["old_pools"].items():
+        r, l = map(int, key.split(":"))
+        old_host.setdefault(r, {})[l] = np.array(arr, dtype=np.uint16)
+    new_host = {}
+    nt = T(*g["new_topo"])
+    for q in range(nt.world):
+        for l in rank_layers(q, g["new_topo"], g["num_layers"]):
+            new_host.setdefault(q, {})[l] = np.full(
+                (2, g["new_num_blocks"], g["new_block_size"], g["num_kv_heads"] // nt.tp, g["head_dim"]),
+                g["sentinel"], np.uint16)
+    log(f"[golden] {name}")
+    plan, src, dst, staging, flags = migrate_all(w, old_t, new_t, old_host, new_host)
+    assert all(f == 0 for f in flags)
+    for key, arr in g["expected_new_pools"].items():
+        q, l = map(int, key.split(":"))
+        np.testing.assert_array_equal(dst[q].host(2)[l], np.array(arr, dtype=np.uint16), err_msg=key)
+    for key, vals in g["expected_staging"].items():
+        r, q = map(int, key.split(":"))
+        np.testing.assert_array_equal(staging[(r, q)].cpu().numpy().view(np.uint16),
+                                      np.array(vals, dtype=np.uint16), err_msg=key)
+
+
+# ---------------------------------------------------------------------------
+# the five workloads (Tiny at full size; the others with a small population)
+# ---------------------------------------------------------------------------
+
+def test_tiny_all_ranks():
+    w = synthkv.TINY
+    check_against_oracle(w, synthkv.make_inputs(w))
+
+
+@pytest.mark.parametrize("name", ["mha7b", "mha13b", "gqa70b", "gqa70b_long"])
+def test_reduced_workload_all_ranks(name):
+    w = synthkv.reduced(synthkv.WORKLOADS[name], num_seqs=5, max_len=300)
+    check_against_oracle(w, synthkv.make_inputs(w))
+
+
+def test_layer_windows_match_whole():
+    w = synthkv.reduced(synthkv.GQA_70B_LONG, num_seqs=3, max_len=200)
+    check_against_oracle(w, synthkv.make_inputs(w), windows=[(0, 1), (1, 7), (7, 40), (40, 41), (41, 80)])
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def _custom(**kw):
+    base = dict(name="edge", num_layers=4, num_kv_heads=8, head_dim=64, elem_bytes=2, dtype="u16",
+                old_block_size=16, new_block_size=16, num_seqs=6, length_law=("uniform", 0, 90),
+                pool_law=("slack", 1.3), old_topo=(2, 1), new_topo=(1, 2), role="all", seed=21)
+    base.update(kw)
+    return synthkv.KVWorkload(**base)
+
+
+EDGE = {
+    "heads_not_nested_reblock": _custom(num_layers=6, num_kv_heads=12, head_dim=32, old_topo=(3, 1),
+                                        new_topo=(2, 3), old_block_size=8, new_block_size=16),
+    "fp8_elements": _custom(elem_bytes=1, old_topo=(4, 1), new_topo=(1, 4)),
+    "fp32_elements": _custom(elem_bytes=4, head_dim=16, old_topo=(1, 2), new_topo=(8, 1)),
+    "odd_row_bytes": _custom(num_kv_heads=4, head_dim=3, old_topo=(2, 1), new_topo=(4, 1)),
+    "identity_2x2": _custom(old_topo=(2, 2), new_topo=(2, 2)),
+    "block_shrink_32_to_8": _custom(old_block_size=32, new_block_size=8, old_topo=(1, 1), new_topo=(2, 2)),
+    "non_power_of_two_block": _custom(old_block_size=12, new_block_size=5, old_topo=(2, 2), new_topo=(4, 1)),
+    "one_token": _custom(num_seqs=1, length_law=("fixed", 1)),
+    "long_single_sequence": _custom(num_seqs=1, length_law=("fixed", 20011), num_layers=2, num_kv_heads=2,
+                                    old_topo=(2, 1), new_topo=(1, 2), head_dim=128),
+    "fragmented_pool": _custom(pool_law=("fragmented", 0.5), num_seqs=12),
+    "all_empty": _custom(length_law=("fixed", 0)),
+    "many_sequences": _custom(num_seqs=1500, length_law=("uniform", 0, 9), num_layers=2),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_case(name):
+    w = EDGE[name]
+    check_against_oracle(w, synthkv.make_inputs(w), log_name=name)
+
+
+def test_padded_table_rows():
+    w = _custom(num_seqs=7)
+    check_against_oracle(w, synthkv.make_inputs(w, row_pad=3), log_name="padded_rows")
+
+
+def test_unpack_from_oracle_staging():
+    """Unpack alone, fed staging the oracle wrote (independent of the pack kernel)."""
+    rk = _rk()
+    w = synthkv.reduced(synthkv.GQA_70B, num_seqs=4, max_len=150)
+    inp = synthkv.make_inputs(w)
+    L, H = w.num_layers, w.num_kv_heads
+    old_host = hostpools.source_pools(w, inp.old_tables)
+    new_host = hostpools.sentinel_pools(w, inp.new_tables)
+    pre = hostpools.copy_pools(new_host)
+    plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
+    pairs = [(p.src, p.dst) for p in plan.pairs]
+    st = oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables,
+                        inp.new_tables, pairs=pairs)
+    staging = {p: torch.from_numpy(oracle.staging_buffer(st[p]).copy()).cuda() for p in pairs}
+    dtn = DeviceTables(inp.new_tables)
+    ws = Workspace(plan)
+    for q in range(plan.info.new_world):
+        dst = RankPool.from_host(pre[q], rank_layers(q, w.new_topo, L), inp.new_tables.num_blocks, q)
+        plan.unpack(q, window_args(plan, staging, q, plan.info.old_world, False, 0, L), dst.arg, dtn.host,
+                    dtn.dev, ws.buf, ws.bytes, stream_handle())
+        torch.cuda.synchronize()
+        assert ws.flag() == 0
+        got = dst.host(2)
+        for l in new_host[q]:
+            np.testing.assert_array_equal(got[l], new_host[q][l])
+
+
+def test_mismatched_device_tables_are_contained():
+    """Device tables that disagree with the host ones must not fault; the flag reports it."""
+    rk = _rk()
+    w = synthkv.reduced(synthkv.TINY, num_seqs=3, max_len=60)
+    inp = synthkv.make_inputs(w)
+    plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
+    old_host = hostpools.source_pools(w, inp.old_tables)
+    src = RankPool.from_host(old_host[0], rank_layers(0, w.old_topo, w.num_layers), inp.old_tables.num_blocks, 0)
+    dto = DeviceTables(inp.old_tables)
+    dto.ids.fill_(1 << 30)                 # every id out of range on the device only
+    pairs = [(p.src, p.dst) for p in plan.pairs]
+    staging = staging_for_pairs(plan, w.seed, pairs)
+    before = {p: b.clone() for p, b in staging.items()}
+    ws = Workspace(plan)
+    plan.pack(0, src.arg, dto.dev, window_args(plan, staging, 0, plan.info.new_world, True, 0, w.num_layers),
+              ws.buf, ws.bytes, stream_handle())
+    torch.cuda.synchronize()
+    assert ws.flag() != 0
+    for p in pairs:                        # nothing was copied
+        assert torch.equal(staging[p], before[p])

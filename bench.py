@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""KV-cache migration benchmark on one MI355X.
+
+One step is the whole hot path for one GPU's share of a topology switch:
+expand the old block tables and pack everything old rank 0 sends (all its
+destinations), then expand the new block tables and unpack everything new
+rank 0 receives (from all its sources).  The staging buffers that other old
+ranks would send to new rank 0 are produced once, untimed, by packing those
+ranks' pools on the same GPU.  All inputs are resident in HBM before timing.
+
+value = algorithmic traffic / step time, with traffic = 2 * (bytes packed +
+bytes unpacked): each payload byte is read once and written once per phase.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_18741_amd", "csrc", "migrate.hip")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gqa70b")
+    ap.add_argument("--cpu-sample-layers", type=int, default=24,
+                    help="layers per new pipeline stage in the oracle's timed sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="only run a plain device copy of this many GiB (for counter scaling), then exit")
+    return ap.parse_args()
+
+
+def source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from committed counter runs, if taken on this kernel source."""
+    try:
+        with open(COUNTERS) as f:
+            c = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if c.get("source_hash") != source_hash():
+        return None
+    k = c.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def copy_calibration(gib: float) -> None:
+    import torch
+    n = int(gib * (1 << 30))
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"copy_bytes_per_launch_read": n, "copy_bytes_per_launch_write": n, "launches": reps,
+                      "ms_per_copy": round(ms, 4), "copy_GBps_read_plus_write": round(2 * n / ms / 1e6, 1)}))
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this build plays one rank's share of the migration on one MI355X "
+              f"and has no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
+        return 2
+    if args.copy_calibration > 0:
+        copy_calibration(args.copy_calibration)
+        return 0
+
+    import numpy as np
+    import torch
+
+    import paper_2606_18741_amd as rk
+    from paper_2606_18741_amd import torch_io as tio
+    import synthkv
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    dev = "cuda:0"
+    w = synthkv.WORKLOADS[args.workload]
+    if w.role == "all":
+        print("bench.py times one rank's share; pick a workload with an (old rank, new rank) role",
+              file=sys.stderr)
+        return 2
+    ro, qn = w.role
+    L, H, D = w.num_layers, w.num_kv_heads, w.head_dim
+    (tpo, ppo), (tpn, ppn) = w.old_topo, w.new_topo
+    inp = synthkv.make_inputs(w)
+    shape = (L, H, D, w.elem_bytes, w.old_block_size, w.new_block_size)
+    plan = rk.Plan(w.old_topo, w.new_topo, shape, rk.HostTables.of(inp.old_tables))
+    W_old, W_new = plan.info.old_world, plan.info.new_world
+    pairs_out = [(p.src, p.dst) for p in plan.pairs if p.src == ro]
+    pairs_in = [(p.src, p.dst) for p in plan.pairs if p.dst == qn]
+    pair_info = {(p.src, p.dst): p for p in plan.pairs}
+    P_pack = sum(pair_info[p].staging_bytes for p in pairs_out)
+    P_unpack = sum(pair_info[p].staging_bytes for p in pairs_in)
+    traffic = 2 * (P_pack + P_unpack)
+    log(f"workload {w.name}: T={plan.info.total_tokens} tokens, old blocks {plan.info.old_live_blocks}, "
+        f"pack {P_pack / 1e9:.2f} GB, unpack {P_unpack / 1e9:.2f} GB")
+
+    def layers_of(rank, tp, pp):
+        per = L // pp
+        return range((rank // tp) * per, (rank // tp + 1) * per)
+
+    dt = synthkv.torch_dtype_for(w.elem_bytes)
+
+    def alloc_layer(tables, tp):
+        return torch.empty((2, tables.num_blocks, tables.block_size, H // tp, D), dtype=dt, device=dev)
+
+    # --- inputs ------------------------------------------------------------
+    t0 = time.time()
+    src_layers = {}
+    for l in layers_of(ro, tpo, ppo):
+        t = alloc_layer(inp.old_tables, tpo)
+        for kv in range(2):
+            synthkv.fill_pool_layer_(t[kv], w.seed, ro, l, kv)
+        src_layers[l] = t
+    src_arg = tio.pool_arg([src_layers[l] for l in layers_of(ro, tpo, ppo)], inp.old_tables.num_blocks)
+    dst_layers = {l: alloc_layer(inp.new_tables, tpn) for l in layers_of(qn, tpn, ppn)}
+    dst_arg = tio.pool_arg([dst_layers[l] for l in layers_of(qn, tpn, ppn)], inp.new_tables.num_blocks)
+    dto = tio.DeviceTables(rk.HostTables.of(inp.old_tables), dev)
+    dtn = tio.DeviceTables(rk.HostTables.of(inp.new_tables), dev)
+    staging = tio.alloc_staging(plan, sorted(set(pairs_out) | set(pairs_in)), dev)
+    ws = tio.workspace(plan, dev)
+    stream = tio.current_stream()
+    torch.cuda.synchronize()
+    log(f"source and destination pools ready ({time.time() - t0:.1f}s)")
+
+    # staging that other old ranks send to new rank qn: pack them once, untimed
+    foreign_host = {}
+    keep_layers = set()
+    if not args.no_cpu_baseline:
+        per_new = L // ppn
+        k = max(1, min(args.cpu_sample_layers, per_new))
+        keep_layers = {s * per_new + i for s in range(ppn) for i in range(k)}
+    # Each foreign source packs its whole share (all its destinations, like the
+    # timed pack of old rank ro), so every pack launch in a profile has one shape.
+    for (r, q) in pairs_in:
+        if r == ro:
+            continue
+        tmp = {}
+        for l in layers_of(r, tpo, ppo):
+            t = alloc_layer(inp.old_tables, tpo)
+            for kv in range(2):
+                synthkv.fill_pool_layer_(t[kv], w.seed, r, l, kv)
+            tmp[l] = t
+            if l in keep_layers and pair_info[(r, q)].layer_begin <= l < pair_info[(r, q)].layer_end:
+                foreign_host[(r, l)] = t.cpu().numpy().view(synthkv.numpy_dtype_for(w.elem_bytes))
+        arg = tio.pool_arg([tmp[l] for l in layers_of(r, tpo, ppo)], inp.old_tables.num_blocks)
+        extra = tio.alloc_staging(plan, [pp for pp in pair_info if pp[0] == r and pp != (r, q)], dev)
+        bufs = dict(extra)
+        bufs[(r, q)] = staging[(r, q)]
+        plan.pack(r, arg, dto.dev, tio.staging_args(bufs, r, W_new, as_src=True), ws, ws.numel(), stream)
+        torch.cuda.synchronize()
+        if tio.workspace_flag(ws) != 0:
+            raise RuntimeError("device tables disagree with host tables")
+        del tmp, arg, extra, bufs
+        torch.cuda.empty_cache()
+    log(f"foreign staging packed ({time.time() - t0:.1f}s)")
+
+    st_out = tio.staging_args(staging, ro, W_new, as_src=True)
+    st_in = tio.staging_args(staging, qn, W_old, as_src=False)
+
+    def step(ev=None):
+        if ev is not None:
+            rk.remp_kv_set_trace_events(ev[0].cuda_event, ev[1].cuda_event)
+        plan.pack(ro, src_arg, dto.dev, st_out, ws, ws.numel(), stream)
+        if ev is not None:
+            rk.remp_kv_set_trace_events(ev[2].cuda_event, ev[3].cuda_event)
+        plan.unpack(qn, st_in, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream)
+        if ev is not None:
+            rk.remp_kv_set_trace_events(None, None)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if tio.workspace_flag(ws) != 0:
+        raise RuntimeError("device tables disagree with host tables")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for e4 in evs:           # torch creates the HIP event on first record; the library re-records it
+        for e in e4:
+            e.record()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / max(args.steps, 1)
+    pack_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    unpack_ms = [e[2].elapsed_time(e[3]) for e in evs]
+    value = traffic / (ms_per_step / 1e3) / 1e9
+    log(f"{args.steps} steps: {ms_per_step:.3f} ms/step, pack kernel {statistics.mean(pack_ms):.3f} ms, "
+        f"unpack kernel {statistics.mean(unpack_ms):.3f} ms, {value:.1f} GB/s")
+
+    pack_avg, unpack_avg = statistics.mean(pack_ms), statistics.mean(unpack_ms)
+    if pack_avg >= unpack_avg:
+        dom, dom_ms, dom_bytes = "pack", pack_avg, 2 * P_pack
+    else:
+        dom, dom_ms, dom_bytes = "unpack", unpack_avg, 2 * P_unpack
+    achieved = dom_bytes / (dom_ms / 1e3) / 1e9
+    roofline = {
+        "bound": "hbm",
+        "kernel": f"copy_slices ({dom})",
+        "achieved": round(achieved, 1),
+        "peak": PEAK_HBM_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / PEAK_HBM_GBS, 4),
+        "traffic": measured_traffic(dom),
+        "algorithmic_bytes_per_launch": dom_bytes,
+        "avg_launch_ms": round(dom_ms, 4),
+    }
+
+    # --- CPU baseline: the oracle on a bounded sample of the same workload ----
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        nd = synthkv.numpy_dtype_for(w.elem_bytes)
+        sample = sorted(keep_layers)
+        old_h = {ro: {l: src_layers[l].cpu().numpy().view(nd) for l in sample if l in src_layers}}
+        for (r, l), a in foreign_host.items():
+            old_h.setdefault(r, {})[l] = a
+        new_h = {qn: {l: np.empty(tuple(dst_layers[l].shape), dtype=nd) for l in sample if l in dst_layers}}
+        want = sorted(set(pairs_out) | set(pairs_in))
+        log(f"oracle on layers {sample} ...")
+        t1 = time.perf_counter()
+        oracle.reshard(old_h, new_h, oracle.Topology(tpo, ppo), oracle.Topology(tpn, ppn), L, H,
+                       inp.old_tables, inp.new_tables, layers=sample, pairs=want)
+        cpu_s = time.perf_counter() - t1
+        moved = 0
+        for key in want:
+            p = pair_info[key]
+            n_l = len([l for l in sample if p.layer_begin <= l < p.layer_end])
+            moved += 2 * n_l * p.slice_bytes * (2 if (key in pairs_out and key in pairs_in) else 1)
+        cpu_value = moved / cpu_s / 1e9
+        cpu = {"value": round(cpu_value, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "seconds": round(cpu_s, 2),
+               "sample": f"layers {sample} of the same workload and role: pack slices of old rank {ro} "
+                         f"and unpack slices of new rank {qn} in those layers ({moved / 1e9:.2f} GB of "
+                         f"traffic by the same definition); NumPy, one thread"}
+        log(f"oracle: {cpu_s:.1f}s, {cpu_value:.2f} GB/s")
+
+    out = {
+        "metric": "KV migration GB/s (pack+unpack) and % of MI355X HBM peak, 70B GQA share",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "pct_of_hbm_peak": round(100 * value / PEAK_HBM_GBS, 2),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name + ": " + w.description,
+            "role": f"old rank {ro} packs for all destinations, new rank {qn} unpacks from all sources",
+            "total_tokens": plan.info.total_tokens,
+            "pack_bytes": P_pack,
+            "unpack_bytes": P_unpack,
+            "traffic_bytes": traffic,
+            "pack_kernel_ms": round(pack_avg, 4),
+            "unpack_kernel_ms": round(unpack_avg, 4),
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -261,13 +261,18 @@ def new_location(l: int, h: int, s: int, t: int, new: Topology, L: int, H: int, 
 
 
 def staging_location(r: int, q: int, l: int, kv: int, h: int, s: int, t: int, old: Topology,
-                     new: Topology, L: int, H: int, D: int, elem_bytes: int, seq_lens) -> int:
-    """Byte offset, in the (r, q) staging buffer, of row (l, kv, s, t, h)."""
-    ps = pair_slices(old, new, L, H)
+                     new: Topology, L: int, H: int, D: int, elem_bytes: int, seq_lens,
+                     slices=None, tok_off=None) -> int:
+    """Byte offset, in the (r, q) staging buffer, of row (l, kv, s, t, h).
+
+    `slices` (pair_slices of the same topologies) and `tok_off` (token_offsets
+    of seq_lens) may be passed in to avoid recomputing them per query.
+    """
+    ps = pair_slices(old, new, L, H) if slices is None else slices
     ls, hs = ps[(r, q)]
     if l not in ls or h not in hs:
         raise ValueError("row is not part of this pair's staging")
-    tok_off = token_offsets(seq_lens)
+    tok_off = token_offsets(seq_lens) if tok_off is None else tok_off
     T = int(tok_off[-1])
     slice_bytes = 2 * T * len(hs) * D * elem_bytes
     row = (kv * T + int(tok_off[s]) + t) * len(hs) + hs.index(h)

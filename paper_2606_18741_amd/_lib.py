@@ -84,7 +84,18 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python paper_2606_18741_amd/build.py` "
                           "(the migration has no fallback path)")
+    # torch carries its own HIP runtime.  Loading torch first lets the library's
+    # libamdhip64.so.7 dependency resolve to that same runtime, so device
+    # pointers, streams and events are shared by one runtime in the process.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
+    runtimes = _mapped_hip_runtimes()
+    if len(runtimes) > 1:
+        raise ImportError("more than one HIP runtime is loaded in this process "
+                          f"({', '.join(runtimes)}); import torch before anything else that loads HIP")
     st = c_int32
     lib.remp_kv_plan.argtypes = [POINTER(Topo), POINTER(Topo), POINTER(Shape), POINTER(BlockTables),
                                  POINTER(c_void_p)]
@@ -115,6 +126,15 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.remp_kv_version.restype = c_char_p
     _lib = lib
     return lib
+
+
+def _mapped_hip_runtimes():
+    """Distinct libamdhip64 files mapped into this process (Linux)."""
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({os.path.realpath(ln.split()[-1]) for ln in f if "libamdhip64" in ln})
+    except OSError:
+        return []
 
 
 def _check(status: int, where: str) -> None:

@@ -58,7 +58,7 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t magic, uint32_
     return static_cast<uint32_t>((t + n) >> shift);
 }
 
-constexpr int kMaxItems = 64;         // slices per copy launch (kernel arguments stay < 4 KiB)
+constexpr int kMaxItems = 96;         // slices per copy launch (kernel arguments stay < 4 KiB)
 constexpr int kMaxDescPerWg = 64;     // block descriptors per workgroup
 constexpr int kCopyThreads = 256;
 constexpr int kScanThreads = 1024;
@@ -84,6 +84,7 @@ struct CopyArgs {
     int32_t block_size;       // paged-side block size
     CopyItem items[kMaxItems];
 };
+static_assert(sizeof(CopyArgs) < 4096, "copy kernel arguments must stay below 4 KiB");
 
 // ---------------------------------------------------------------------------
 // expansion: block tables -> one descriptor per live block

@@ -28,7 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
-COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
+COUNTERS = os.path.join(ROOT, "profiles", "copy_slices_gqa70b_hbm_counters.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_18741_amd", "csrc", "migrate.hip")
 
 

@@ -59,8 +59,16 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t magic, uint32_
 }
 
 constexpr int kMaxItems = 96;         // slices per copy launch (kernel arguments stay < 4 KiB)
-constexpr int kMaxDescPerWg = 64;     // block descriptors per workgroup
-constexpr int kCopyThreads = 256;
+constexpr int kMaxUnitsPerWg = 128;   // (block, K or V) units per workgroup
+// Copy launch policies (measured on MI355X).  Small (block, K/V) units, as
+// with GQA head rows of 256 B, run fastest as many small workgroups, each
+// moving one unit; large units (MHA rows of several KiB) prefer wider
+// workgroups that move about 64 KiB.
+constexpr int64_t kSmallUnitBytes = 16 * 1024;   // units up to this size use the small policy
+constexpr int kSmallThreads = 128, kSmallUnroll = 4;
+constexpr int64_t kSmallWgBytes = 4 * 1024;
+constexpr int kLargeThreads = 256, kLargeUnroll = 8;
+constexpr int64_t kLargeWgBytes = 64 * 1024;
 constexpr int kScanThreads = 1024;
 
 struct CopyItem {
@@ -79,7 +87,7 @@ struct CopyArgs {
     int64_t block_stride;     // bytes per block on the paged side
     int64_t total_tokens;     // T: a slice's V part starts T * row_bytes after its K part
     int32_t n_desc;
-    int32_t descs_per_wg;
+    int32_t units_per_wg;
     int32_t row_stride;       // bytes per token row on the paged side (all local heads)
     int32_t block_size;       // paged-side block size
     CopyItem items[kMaxItems];
@@ -222,23 +230,24 @@ template <> struct VecT<4> { typedef unsigned int type; };
 template <> struct VecT<2> { typedef unsigned short type; };
 template <> struct VecT<1> { typedef unsigned char type; };
 
-template <int VEC, bool PACK, int UNROLL>
-__global__ __launch_bounds__(kCopyThreads) void copy_slices(const CopyArgs args) {
+template <int VEC, bool PACK, int THREADS, int UNROLL>
+__global__ __launch_bounds__(THREADS) void copy_slices(const CopyArgs args) {
     typedef typename VecT<VEC>::type V;
-    __shared__ uint64_t s_paged[2 * kMaxDescPerWg];
-    __shared__ uint64_t s_stage[2 * kMaxDescPerWg];
-    __shared__ int32_t s_n[2 * kMaxDescPerWg];
+    __shared__ uint64_t s_paged[kMaxUnitsPerWg];
+    __shared__ uint64_t s_stage[kMaxUnitsPerWg];
+    __shared__ int32_t s_n[kMaxUnitsPerWg];
 
     const CopyItem& it = args.items[blockIdx.y];
-    const int32_t d0 = static_cast<int32_t>(blockIdx.x) * args.descs_per_wg;
-    const int32_t nd = min(args.descs_per_wg, args.n_desc - d0);
+    const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
+    const int32_t nu = min(args.units_per_wg, 2 * args.n_desc - u0);
     const int tid = threadIdx.x;
     const uint64_t kv_stride = static_cast<uint64_t>(args.total_tokens) * it.row_bytes;
 
-    // unit u = (descriptor d0 + u/2, kv = u%2): base addresses of its two sides
-    for (int u = tid; u < 2 * nd; u += kCopyThreads) {
-        const BlockDesc d = args.desc[d0 + (u >> 1)];
-        const int kv = u & 1;
+    // unit u0 + u = (descriptor (u0 + u) / 2, kv = (u0 + u) % 2): base addresses of its two sides
+    for (int u = tid; u < nu; u += THREADS) {
+        const int32_t g = u0 + u;
+        const BlockDesc d = args.desc[g >> 1];
+        const int kv = g & 1;
         s_paged[u] = (kv ? it.paged_v : it.paged_k) + static_cast<uint64_t>(d.block) * args.block_stride;
         s_stage[u] = it.stage + kv * kv_stride + static_cast<uint64_t>(d.tok) * it.row_bytes;
         s_n[u] = d.n;
@@ -247,16 +256,16 @@ __global__ __launch_bounds__(kCopyThreads) void copy_slices(const CopyArgs args)
 
     const uint32_t vpr = it.row_bytes / VEC;
     const uint32_t unit = static_cast<uint32_t>(args.block_size) * vpr;
-    const uint32_t total = static_cast<uint32_t>(2 * nd) * unit;
+    const uint32_t total = static_cast<uint32_t>(nu) * unit;
     const uint32_t row_stride = static_cast<uint32_t>(args.row_stride);
 
-    for (uint32_t base = tid; base < total; base += kCopyThreads * UNROLL) {
+    for (uint32_t base = tid; base < total; base += THREADS * UNROLL) {
         V r[UNROLL];
         uint64_t dst[UNROLL];
         bool ok[UNROLL];
 #pragma unroll
         for (int j = 0; j < UNROLL; ++j) {
-            const uint32_t idx = base + j * kCopyThreads;
+            const uint32_t idx = base + j * THREADS;
             ok[j] = false;
             dst[j] = 0;
             if (idx < total) {
@@ -324,8 +333,13 @@ static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables&
 }
 
 template <int VEC, bool PACK>
-static void launch_copy_vec(const CopyArgs& a, dim3 grid, hipStream_t stream) {
-    hipLaunchKernelGGL((copy_slices<VEC, PACK, 8>), grid, dim3(kCopyThreads), 0, stream, a);
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_t stream) {
+    if (small)
+        hipLaunchKernelGGL((copy_slices<VEC, PACK, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((copy_slices<VEC, PACK, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0,
+                           stream, a);
 }
 
 template <bool PACK>
@@ -333,6 +347,7 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
                                int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
                                hipStream_t stream) {
     if (slices.empty() || n_desc == 0) return REMP_OK;
+    if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
     // widest vector every address and stride is aligned to
     uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(row_stride) | 16u;
     uint32_t max_row = 0;
@@ -342,12 +357,13 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
         max_row = std::max(max_row, s.row_bytes);
     }
     const int vec = static_cast<int>(bits & (~bits + 1));   // lowest set bit, <= 16
-    const int64_t target = env_int("REMP_KV_WG_BYTES", 64 * 1024);
-    const int64_t per_desc = 2 * static_cast<int64_t>(bs) * max_row;
-    int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxDescPerWg, target / per_desc)));
+    const int64_t per_unit = static_cast<int64_t>(bs) * max_row;
+    const bool small = per_unit <= kSmallUnitBytes;
+    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kSmallWgBytes : kLargeWgBytes));
+    int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
     // the flattened per-workgroup index must stay below 2^32
-    while (C > 1 && static_cast<uint64_t>(2) * C * bs * (max_row / vec) >= (uint64_t(1) << 32)) C >>= 1;
-    if (static_cast<uint64_t>(2) * bs * (max_row / vec) >= (uint64_t(1) << 32))
+    while (C > 1 && static_cast<uint64_t>(C) * bs * (max_row / vec) >= (uint64_t(1) << 32)) C >>= 1;
+    if (static_cast<uint64_t>(bs) * (max_row / vec) >= (uint64_t(1) << 32))
         return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^32 vectors");
 
     CopyArgs a;
@@ -356,10 +372,10 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     a.block_stride = block_stride;
     a.total_tokens = p.total_tokens;
     a.n_desc = static_cast<int32_t>(n_desc);
-    a.descs_per_wg = C;
+    a.units_per_wg = C;
     a.row_stride = row_stride;
     a.block_size = bs;
-    const int64_t gx = (n_desc + C - 1) / C;
+    const int64_t gx = (2 * n_desc + C - 1) / C;
     if (gx > 0x7FFFFFFF) return fail(REMP_E_UNSUPPORTED, "too many block descriptors for one launch");
 
     if (g_trace_start) {
@@ -383,11 +399,11 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
         }
         const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
         switch (vec) {
-            case 16: launch_copy_vec<16, PACK>(a, grid, stream); break;
-            case 8: launch_copy_vec<8, PACK>(a, grid, stream); break;
-            case 4: launch_copy_vec<4, PACK>(a, grid, stream); break;
-            case 2: launch_copy_vec<2, PACK>(a, grid, stream); break;
-            default: launch_copy_vec<1, PACK>(a, grid, stream); break;
+            case 16: launch_copy_vec<16, PACK>(a, grid, small, stream); break;
+            case 8: launch_copy_vec<8, PACK>(a, grid, small, stream); break;
+            case 4: launch_copy_vec<4, PACK>(a, grid, small, stream); break;
+            case 2: launch_copy_vec<2, PACK>(a, grid, small, stream); break;
+            default: launch_copy_vec<1, PACK>(a, grid, small, stream); break;
         }
         if (remp_status st = hip_check(hipGetLastError(), PACK ? "pack launch" : "unpack launch")) return st;
     }

@@ -226,6 +226,38 @@ def main() -> int:
     log(f"{args.steps} steps: {ms_per_step:.3f} ms/step, pack kernel {statistics.mean(pack_ms):.3f} ms, "
         f"unpack kernel {statistics.mean(unpack_ms):.3f} ms, {value:.1f} GB/s")
 
+    # --- the same share with the local fast path (slices old rank ro keeps as new
+    # rank qn go pool to pool; the rest through staging), timed the same way
+    local = None
+    if ro == qn and (ro, qn) in pair_info:
+        P_local = pair_info[(ro, qn)].staging_bytes
+        st_out_r = tio.staging_args({k: v for k, v in staging.items() if k[0] == ro and k[1] != ro}, ro, W_new, True)
+        st_in_r = tio.staging_args({k: v for k, v in staging.items() if k[1] == qn and k[0] != qn}, qn, W_old, False)
+
+        def step_local():
+            plan.pack(ro, src_arg, dto.dev, st_out_r, ws, ws.numel(), stream, flags=rk.REMP_KV_SKIP_LOCAL)
+            plan.copy_local(ro, src_arg, dto.dev, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream)
+            plan.unpack(qn, st_in_r, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream, flags=rk.REMP_KV_SKIP_LOCAL)
+
+        for _ in range(args.warmup):
+            step_local()
+        torch.cuda.synchronize()
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record()
+        for _ in range(args.steps):
+            step_local()
+        a1.record()
+        torch.cuda.synchronize()
+        if tio.workspace_flag(ws) != 0:
+            raise RuntimeError("device tables disagree with host tables")
+        ms_local = a0.elapsed_time(a1) / max(args.steps, 1)
+        moved = traffic - 2 * P_local
+        local = {"ms_per_step": round(ms_local, 4), "speedup_vs_staged": round(ms_per_step / ms_local, 3),
+                 "hbm_traffic_bytes": moved, "hbm_GBps": round(moved / (ms_local / 1e3) / 1e9, 1),
+                 "local_bytes": P_local}
+        log(f"local fast path: {ms_local:.3f} ms/step ({ms_per_step / ms_local:.2f}x), "
+            f"{local['hbm_GBps']} GB/s of HBM traffic")
+
     pack_avg, unpack_avg = statistics.mean(pack_ms), statistics.mean(unpack_ms)
     if pack_avg >= unpack_avg:
         dom, dom_ms, dom_bytes = "pack", pack_avg, 2 * P_pack
@@ -298,6 +330,7 @@ def main() -> int:
             "unpack_kernel_ms": round(unpack_avg, 4),
         },
         "roofline": roofline,
+        "local_fast_path": local,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

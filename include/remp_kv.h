@@ -148,6 +148,15 @@ typedef struct {
 
 typedef struct remp_kv_plan_s remp_kv_plan_t;
 
+/* Flags of remp_kv_pack and remp_kv_unpack. */
+enum {
+    /* Leave out the slices whose peer is the calling rank itself (the same
+     * global rank id in the old and the new topology).  Those slices stay on
+     * the worker (Section 3.4.3, local copy); move them with
+     * remp_kv_copy_local instead of staging them. */
+    REMP_KV_SKIP_LOCAL = 1u
+};
+
 /* Build the migration plan for T_old -> T_new (Section 3.4.2, Algorithm 1:
  * for every layer, intersect each new tensor rank's head range with each old
  * tensor rank's; every non-empty overlap is one send item of the old rank and
@@ -190,12 +199,13 @@ REMP_API remp_status remp_kv_workspace_bytes(const remp_kv_plan_t* plan, int64_t
  * nothing in the window may be {NULL, 0}.  Never writes src (the source
  * topology stays intact until the caller commits, Section 3.7).
  * old_tables: device copy of the tables given to remp_kv_plan.
+ * flags: 0 or REMP_KV_SKIP_LOCAL (then staging[old_rank] is not used).
  * Everything is validated before anything is enqueued; on error nothing is. */
 REMP_API remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank,
                          int32_t layer_begin, int32_t layer_end,
                          const remp_kv_pool* src, const remp_dev_tables* old_tables,
                          const remp_buffer* staging,
-                         void* workspace, int64_t workspace_bytes, hipStream_t stream);
+                         void* workspace, int64_t workspace_bytes, uint32_t flags, hipStream_t stream);
 
 /* Unpack (Section 3.4.2 receive side, Section 3.4.4 per layer window): for
  * every slice new_rank receives whose layer lies in [layer_begin, layer_end),
@@ -207,17 +217,39 @@ REMP_API remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank,
  * long enough, ids in [0, new_tables->num_blocks), no id used twice
  * (REMP_E_INVALID), enough blocks for the live cache (REMP_E_CAPACITY), and
  * dst->num_blocks >= new_tables->num_blocks (REMP_E_SIZE).
- * new_dev_tables: device copy of new_tables. */
+ * new_dev_tables: device copy of new_tables.
+ * flags: 0 or REMP_KV_SKIP_LOCAL (then staging[new_rank] is not used). */
 REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank,
                            int32_t layer_begin, int32_t layer_end,
                            const remp_buffer* staging,
                            const remp_kv_pool* dst, const remp_block_tables* new_tables,
                            const remp_dev_tables* new_dev_tables,
-                           void* workspace, int64_t workspace_bytes, hipStream_t stream);
+                           void* workspace, int64_t workspace_bytes, uint32_t flags, hipStream_t stream);
 
-/* Measurement hook: while set (non-NULL), the calling thread's pack and unpack
- * calls record `start` immediately before and `stop` immediately after their
- * copy kernel(s) on the call's stream.  Pass NULL, NULL to clear. */
+/* Local copy (Section 3.4.3: when a slice's source and destination are the
+ * same worker it is copied locally instead of transferred): for the slices
+ * that `rank` sends to itself (same global rank id in both topologies) in
+ * layers [layer_begin, layer_end), copy the live rows straight from src (the
+ * rank's old pool, addressed by the planned old tables) into dst (its new
+ * pool, addressed by new_tables), without staging.  Together with pack and
+ * unpack called with REMP_KV_SKIP_LOCAL this yields the same new pool as a
+ * staged migration while moving the local share once instead of twice.
+ * rank must exist in both topologies.  src and dst storage must not overlap
+ * (checked per layer, REMP_E_INVALID).  new_tables are validated as in
+ * remp_kv_unpack.  old_tables / new_dev_tables: device copies of the tables.
+ * The workspace is the one remp_kv_workspace_bytes sizes; nothing is enqueued
+ * on error. */
+REMP_API remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank,
+                               int32_t layer_begin, int32_t layer_end,
+                               const remp_kv_pool* src, const remp_dev_tables* old_tables,
+                               const remp_kv_pool* dst, const remp_block_tables* new_tables,
+                               const remp_dev_tables* new_dev_tables,
+                               void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* Measurement hook: while set (non-NULL), the calling thread's pack, unpack
+ * and copy_local calls record `start` immediately before and `stop`
+ * immediately after their copy kernel(s) on the call's stream.  Pass NULL,
+ * NULL to clear. */
 REMP_API void remp_kv_set_trace_events(hipEvent_t start, hipEvent_t stop);
 
 REMP_API const char* remp_status_string(remp_status status);

@@ -23,9 +23,11 @@ STATUS = {0: "REMP_OK", -1: "REMP_E_INVALID", -2: "REMP_E_UNSUPPORTED", -3: "REM
 # every symbol include/remp_kv.h declares
 EXPORTED = (
     "remp_kv_plan", "remp_kv_plan_destroy", "remp_kv_plan_get_info", "remp_kv_plan_get_pair",
-    "remp_kv_plan_query", "remp_kv_workspace_bytes", "remp_kv_pack", "remp_kv_unpack",
+    "remp_kv_plan_query", "remp_kv_workspace_bytes", "remp_kv_pack", "remp_kv_unpack", "remp_kv_copy_local",
     "remp_kv_set_trace_events", "remp_status_string", "remp_last_error", "remp_kv_version",
 )
+
+REMP_KV_SKIP_LOCAL = 1
 
 
 class RempError(RuntimeError):
@@ -111,11 +113,16 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.remp_kv_workspace_bytes.argtypes = [c_void_p, POINTER(c_int64)]
     lib.remp_kv_workspace_bytes.restype = st
     lib.remp_kv_pack.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(Pool), POINTER(DevTables),
-                                 POINTER(Buffer), c_void_p, c_int64, c_void_p]
+                                 POINTER(Buffer), c_void_p, c_int64, ctypes.c_uint32, c_void_p]
     lib.remp_kv_pack.restype = st
     lib.remp_kv_unpack.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(Buffer), POINTER(Pool),
-                                   POINTER(BlockTables), POINTER(DevTables), c_void_p, c_int64, c_void_p]
+                                   POINTER(BlockTables), POINTER(DevTables), c_void_p, c_int64, ctypes.c_uint32,
+                                   c_void_p]
     lib.remp_kv_unpack.restype = st
+    lib.remp_kv_copy_local.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(Pool), POINTER(DevTables),
+                                       POINTER(Pool), POINTER(BlockTables), POINTER(DevTables), c_void_p, c_int64,
+                                       c_void_p]
+    lib.remp_kv_copy_local.restype = st
     lib.remp_kv_set_trace_events.argtypes = [c_void_p, c_void_p]
     lib.remp_kv_set_trace_events.restype = None
     lib.remp_status_string.argtypes = [c_int32]
@@ -153,6 +160,13 @@ def _ptr(x) -> Optional[int]:
     if hasattr(x, "data_ptr"):
         return int(x.data_ptr())
     return int(x)
+
+
+def _ref(x):
+    """byref of a wrapper's C struct (or of a ctypes struct); None stays NULL."""
+    if x is None:
+        return None
+    return byref(x.c) if hasattr(x, "c") else byref(x)
 
 
 class HostTables:
@@ -248,17 +262,26 @@ def remp_kv_workspace_bytes(plan) -> int:
 
 
 def remp_kv_pack(plan, old_rank: int, layer_begin: int, layer_end: int, src: PoolArg, old_dev_tables: DevTables,
-                 staging, workspace, workspace_bytes: int, stream: int) -> None:
-    _check(load().remp_kv_pack(plan, old_rank, layer_begin, layer_end, byref(src.c), byref(old_dev_tables),
-                               staging, _ptr(workspace), int(workspace_bytes), c_void_p(stream)), "remp_kv_pack")
+                 staging, workspace, workspace_bytes: int, flags: int, stream: int) -> None:
+    _check(load().remp_kv_pack(plan, old_rank, layer_begin, layer_end, _ref(src), _ref(old_dev_tables),
+                               staging, _ptr(workspace), int(workspace_bytes), int(flags), c_void_p(stream)),
+           "remp_kv_pack")
 
 
 def remp_kv_unpack(plan, new_rank: int, layer_begin: int, layer_end: int, staging, dst: PoolArg,
                    new_tables: HostTables, new_dev_tables: DevTables, workspace, workspace_bytes: int,
-                   stream: int) -> None:
-    _check(load().remp_kv_unpack(plan, new_rank, layer_begin, layer_end, staging, byref(dst.c),
-                                 byref(new_tables.c), byref(new_dev_tables), _ptr(workspace),
-                                 int(workspace_bytes), c_void_p(stream)), "remp_kv_unpack")
+                   flags: int, stream: int) -> None:
+    _check(load().remp_kv_unpack(plan, new_rank, layer_begin, layer_end, staging, _ref(dst),
+                                 _ref(new_tables), _ref(new_dev_tables), _ptr(workspace),
+                                 int(workspace_bytes), int(flags), c_void_p(stream)), "remp_kv_unpack")
+
+
+def remp_kv_copy_local(plan, rank: int, layer_begin: int, layer_end: int, src: PoolArg, old_dev_tables: DevTables,
+                       dst: PoolArg, new_tables: HostTables, new_dev_tables: DevTables, workspace,
+                       workspace_bytes: int, stream: int) -> None:
+    _check(load().remp_kv_copy_local(plan, rank, layer_begin, layer_end, _ref(src), _ref(old_dev_tables),
+                                     _ref(dst), _ref(new_tables), _ref(new_dev_tables), _ptr(workspace),
+                                     int(workspace_bytes), c_void_p(stream)), "remp_kv_copy_local")
 
 
 def remp_kv_set_trace_events(start: Optional[int], stop: Optional[int]) -> None:
@@ -310,11 +333,18 @@ class Plan:
         return remp_kv_workspace_bytes(self.handle)
 
     def pack(self, old_rank, src: PoolArg, old_dev_tables: DevTables, staging, workspace, workspace_bytes,
-             stream, layer_begin: int = 0, layer_end: Optional[int] = None) -> None:
+             stream, layer_begin: int = 0, layer_end: Optional[int] = None, flags: int = 0) -> None:
         remp_kv_pack(self.handle, old_rank, layer_begin, self.num_layers if layer_end is None else layer_end,
-                     src, old_dev_tables, staging, workspace, workspace_bytes, stream)
+                     src, old_dev_tables, staging, workspace, workspace_bytes, flags, stream)
 
     def unpack(self, new_rank, staging, dst: PoolArg, new_tables: HostTables, new_dev_tables: DevTables,
-               workspace, workspace_bytes, stream, layer_begin: int = 0, layer_end: Optional[int] = None) -> None:
+               workspace, workspace_bytes, stream, layer_begin: int = 0, layer_end: Optional[int] = None,
+               flags: int = 0) -> None:
         remp_kv_unpack(self.handle, new_rank, layer_begin, self.num_layers if layer_end is None else layer_end,
-                       staging, dst, new_tables, new_dev_tables, workspace, workspace_bytes, stream)
+                       staging, dst, new_tables, new_dev_tables, workspace, workspace_bytes, flags, stream)
+
+    def copy_local(self, rank, src: PoolArg, old_dev_tables: DevTables, dst: PoolArg, new_tables: HostTables,
+                   new_dev_tables: DevTables, workspace, workspace_bytes, stream, layer_begin: int = 0,
+                   layer_end: Optional[int] = None) -> None:
+        remp_kv_copy_local(self.handle, rank, layer_begin, self.num_layers if layer_end is None else layer_end,
+                           src, old_dev_tables, dst, new_tables, new_dev_tables, workspace, workspace_bytes, stream)

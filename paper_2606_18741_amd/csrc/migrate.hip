@@ -29,12 +29,13 @@ namespace remp {
 // ---------------------------------------------------------------------------
 
 // One live block of one sequence: physical block id, position of its first
-// token on the sequence-major token axis, number of live tokens in it.
+// token on the sequence-major token axis, number of live tokens in it, and
+// the sequence it belongs to.
 struct BlockDesc {
     int32_t block;
     int32_t tok;
     int32_t n;
-    int32_t pad;
+    int32_t seq;
 };
 
 // Division by a runtime constant d for any 32-bit numerator (Granlund and
@@ -101,7 +102,7 @@ static_assert(sizeof(CopyArgs) < 4096, "copy kernel arguments must stay below 4 
 // Exclusive prefix sums of tokens and of blocks per sequence (one workgroup,
 // wave64 shuffle scans combined through LDS, carried across chunks of 1024).
 __global__ __launch_bounds__(kScanThreads) void expand_scan(const int32_t* __restrict__ lens, int32_t S,
-                                                           int32_t bs, int32_t* __restrict__ flag,
+                                                           int32_t bs, int32_t reset_flag, int32_t* __restrict__ flag,
                                                            int32_t* __restrict__ tok_off,
                                                            int32_t* __restrict__ blk_off) {
     __shared__ int64_t wave_tok[kScanThreads / 64];
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(kScanThreads) void expand_scan(const int32_t* __res
     if (tid == 0) {
         carry[0] = 0;
         carry[1] = 0;
-        *flag = 0;
+        if (reset_flag) *flag = 0;
     }
     __syncthreads();
     bool bad = false;
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
             const int64_t rest = n - j * bs;
             const int64_t cnt = rest < bs ? rest : bs;
             ok = id >= 0 && id < num_blocks && cnt > 0 && tok >= 0 && tok + cnt <= total_tokens;
-            if (ok) d = BlockDesc{static_cast<int32_t>(id), static_cast<int32_t>(tok), static_cast<int32_t>(cnt), 0};
+            if (ok) d = BlockDesc{static_cast<int32_t>(id), static_cast<int32_t>(tok), static_cast<int32_t>(cnt), s};
         }
     }
     if (!ok) *flag = 1;
@@ -289,6 +290,115 @@ __global__ __launch_bounds__(THREADS) void copy_slices(const CopyArgs args) {
     }
 }
 
+
+// Local copy (a slice whose old and new owner is the same rank): a unit is
+// (new block, K or V); the prologue resolves every row of the unit's live
+// tokens to its old (block, slot) through the old descriptors, so the main
+// loop is a row-gather with one LDS lookup per vector.
+constexpr int kMaxLocalItems = 64;
+constexpr int kMaxLocalRows = 1024;   // (unit, row) source addresses per workgroup
+
+struct LocalItem {
+    uint64_t src_k, src_v;   // old storage of the layer, offset to the slice's first head
+    uint64_t dst_k, dst_v;   // new storage of the layer, offset to the slice's first head
+    uint32_t row_bytes;
+    uint32_t vpr_magic;
+    uint32_t unit_magic;
+    uint16_t vpr_shift;
+    uint16_t unit_shift;
+};
+
+struct LocalArgs {
+    const BlockDesc* new_desc;
+    const BlockDesc* old_desc;
+    const int32_t* tok_off;       // first token of each sequence on the token axis
+    const int32_t* old_blk_off;   // first old descriptor of each sequence
+    int32_t* flag;
+    int64_t old_block_stride, new_block_stride;
+    int32_t n_new_desc, n_old_desc;
+    int32_t units_per_wg;
+    int32_t old_row_stride, new_row_stride;
+    int32_t old_block_size, new_block_size;
+    LocalItem items[kMaxLocalItems];
+};
+static_assert(sizeof(LocalArgs) < 4096, "local copy kernel arguments must stay below 4 KiB");
+
+template <int VEC, int THREADS, int UNROLL>
+__global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
+    typedef typename VecT<VEC>::type V;
+    __shared__ uint64_t s_dst[kMaxUnitsPerWg];
+    __shared__ int32_t s_n[kMaxUnitsPerWg];
+    __shared__ uint64_t s_src[kMaxLocalRows];
+
+    const LocalItem& it = args.items[blockIdx.y];
+    const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
+    const int32_t nu = min(args.units_per_wg, 2 * args.n_new_desc - u0);
+    const int tid = threadIdx.x;
+    const int32_t bn = args.new_block_size, bo = args.old_block_size;
+
+    for (int u = tid; u < nu; u += THREADS) {
+        const int32_t g = u0 + u;
+        const BlockDesc d = args.new_desc[g >> 1];
+        s_dst[u] = ((g & 1) ? it.dst_v : it.dst_k) + static_cast<uint64_t>(d.block) * args.new_block_stride;
+        s_n[u] = d.n;
+    }
+    for (int i = tid; i < nu * bn; i += THREADS) {
+        const int32_t u = i / bn, r = i - u * bn;
+        const int32_t g = u0 + u;
+        const BlockDesc d = args.new_desc[g >> 1];
+        uint64_t a = 0;
+        if (r < d.n) {
+            const int32_t t = d.tok - args.tok_off[d.seq] + r;          // token within its sequence
+            const int32_t ob = args.old_blk_off[d.seq] + t / bo;
+            const int32_t slot = t - (t / bo) * bo;
+            bool ok = ob >= 0 && ob < args.n_old_desc;
+            BlockDesc od{0, 0, 0, 0};
+            if (ok) {
+                od = args.old_desc[ob];
+                ok = od.seq == d.seq && slot < od.n;
+            }
+            if (ok)
+                a = ((g & 1) ? it.src_v : it.src_k) + static_cast<uint64_t>(od.block) * args.old_block_stride +
+                    static_cast<uint64_t>(slot) * args.old_row_stride;
+            else
+                *args.flag = 1;
+        }
+        s_src[i] = a;
+    }
+    __syncthreads();
+
+    const uint32_t vpr = it.row_bytes / VEC;
+    const uint32_t unit = static_cast<uint32_t>(bn) * vpr;
+    const uint32_t total = static_cast<uint32_t>(nu) * unit;
+    const uint32_t new_row_stride = static_cast<uint32_t>(args.new_row_stride);
+    for (uint32_t base = tid; base < total; base += THREADS * UNROLL) {
+        V r[UNROLL];
+        uint64_t dst[UNROLL];
+        bool ok[UNROLL];
+#pragma unroll
+        for (int j = 0; j < UNROLL; ++j) {
+            const uint32_t idx = base + j * THREADS;
+            ok[j] = false;
+            dst[j] = 0;
+            if (idx < total) {
+                const uint32_t u = fast_div(idx, it.unit_magic, it.unit_shift);
+                const uint32_t rem = idx - u * unit;
+                const uint32_t row = fast_div(rem, it.vpr_magic, it.vpr_shift);
+                const uint32_t c = rem - row * vpr;
+                const uint64_t src_row = s_src[u * bn + row];
+                if (static_cast<int32_t>(row) < s_n[u] && src_row != 0) {
+                    dst[j] = s_dst[u] + static_cast<uint64_t>(row) * new_row_stride + c * VEC;
+                    r[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(src_row + c * VEC));
+                    ok[j] = true;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < UNROLL; ++j)
+            if (ok[j]) __builtin_nontemporal_store(r[j], reinterpret_cast<V*>(dst[j]));
+    }
+}
+
 // ---------------------------------------------------------------------------
 // host launch code
 // ---------------------------------------------------------------------------
@@ -312,15 +422,16 @@ static remp_status hip_check(hipError_t e, const char* what) {
     return fail(REMP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Enqueue expansion of `tables` into descriptors in the workspace.
+// Enqueue expansion of `tables` into the workspace areas at scan_off / desc_off.
 static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables& dt, int32_t bs, int64_t nnz,
-                                 int64_t num_blocks, int64_t n_desc, char* ws, hipStream_t stream) {
+                                 int64_t num_blocks, int64_t n_desc, char* ws, int64_t scan_off, int64_t desc_off,
+                                 bool reset_flag, hipStream_t stream) {
     int32_t* flag = reinterpret_cast<int32_t*>(ws);
-    int32_t* tok_off = reinterpret_cast<int32_t*>(ws + 256);
+    int32_t* tok_off = reinterpret_cast<int32_t*>(ws + scan_off);
     int32_t* blk_off = tok_off + (p.num_seqs + 1);
-    BlockDesc* desc = reinterpret_cast<BlockDesc*>(ws + workspace_desc_offset(p));
-    hipLaunchKernelGGL(expand_scan, dim3(1), dim3(kScanThreads), 0, stream, dt.seq_lens, p.num_seqs, bs, flag,
-                       tok_off, blk_off);
+    BlockDesc* desc = reinterpret_cast<BlockDesc*>(ws + desc_off);
+    hipLaunchKernelGGL(expand_scan, dim3(1), dim3(kScanThreads), 0, stream, dt.seq_lens, p.num_seqs, bs,
+                       reset_flag ? 1 : 0, flag, tok_off, blk_off);
     if (remp_status st = hip_check(hipGetLastError(), "expand_scan launch")) return st;
     if (n_desc > 0) {
         const int64_t blocks = (n_desc + 255) / 256;
@@ -345,7 +456,7 @@ static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_
 template <bool PACK>
 static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSlice>& slices, int64_t n_desc,
                                int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
-                               hipStream_t stream) {
+                               int64_t desc_off, hipStream_t stream) {
     if (slices.empty() || n_desc == 0) return REMP_OK;
     if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
     // widest vector every address and stride is aligned to
@@ -368,7 +479,7 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
 
     CopyArgs a;
     std::memset(&a, 0, sizeof(a));
-    a.desc = reinterpret_cast<const BlockDesc*>(ws + workspace_desc_offset(p));
+    a.desc = reinterpret_cast<const BlockDesc*>(ws + desc_off);
     a.block_stride = block_stride;
     a.total_tokens = p.total_tokens;
     a.n_desc = static_cast<int32_t>(n_desc);
@@ -415,18 +526,23 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
 
 static bool aligned(const void* p, int64_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-static remp_status check_common(const remp_kv_plan_t* plan, int32_t l0, int32_t l1, const remp_kv_pool* pool,
-                                const remp_buffer* staging, void* ws, int64_t ws_bytes, int32_t layers_per_rank) {
-    if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+static remp_status check_window(const remp_kv_plan_t* plan, int32_t l0, int32_t l1) {
     if (l0 < 0 || l1 < l0 || l1 > plan->shape.num_layers)
         return fail(REMP_E_RANGE, "layer window [" + std::to_string(l0) + ", " + std::to_string(l1) +
                                       ") outside [0, " + std::to_string(plan->shape.num_layers) + "]");
-    if (!pool) return fail(REMP_E_INVALID, "pool is NULL");
+    return REMP_OK;
+}
+
+static remp_status check_pool(const remp_kv_pool* pool, int32_t layers_per_rank, const char* what) {
+    if (!pool) return fail(REMP_E_INVALID, std::string(what) + " pool is NULL");
     if (pool->num_layers != layers_per_rank)
-        return fail(REMP_E_INVALID, "pool has " + std::to_string(pool->num_layers) + " layers, the rank holds " +
-                                        std::to_string(layers_per_rank));
-    if (!pool->k || !pool->v) return fail(REMP_E_INVALID, "pool pointer arrays are NULL");
-    if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
+        return fail(REMP_E_INVALID, std::string(what) + " pool has " + std::to_string(pool->num_layers) +
+                                        " layers, the rank holds " + std::to_string(layers_per_rank));
+    if (!pool->k || !pool->v) return fail(REMP_E_INVALID, std::string(what) + " pool pointer arrays are NULL");
+    return REMP_OK;
+}
+
+static remp_status check_workspace(const remp_kv_plan_t* plan, void* ws, int64_t ws_bytes) {
     if (!ws) return fail(REMP_E_INVALID, "workspace is NULL");
     if (!aligned(ws, 256)) return fail(REMP_E_ALIGN, "workspace is not 256-byte aligned");
     if (ws_bytes < workspace_bytes(*plan))
@@ -435,18 +551,73 @@ static remp_status check_common(const remp_kv_plan_t* plan, int32_t l0, int32_t 
     return REMP_OK;
 }
 
+static remp_status check_dev_tables(const remp_kv_plan_t* plan, const remp_dev_tables* dt, int64_t nnz,
+                                    const char* what) {
+    if (!dt) return fail(REMP_E_INVALID, std::string("device ") + what + " tables are NULL");
+    if (plan->num_seqs > 0 && (!dt->seq_lens || !dt->row_offsets))
+        return fail(REMP_E_INVALID, std::string("device ") + what + " table arrays are NULL");
+    if (nnz > 0 && !dt->block_ids) return fail(REMP_E_INVALID, std::string("device ") + what + " block ids are NULL");
+    return REMP_OK;
+}
+
+// New tables describe the planned sequences, every row is long enough, every
+// live id is in range and used once, and the pool can hold the live cache.
+static remp_status check_new_tables(const remp_kv_plan_t* plan, const remp_block_tables* nt,
+                                    const remp_kv_pool* dst, int64_t* nnz_out) {
+    if (!nt) return fail(REMP_E_INVALID, "new tables are NULL");
+    const remp_block_tables& t = *nt;
+    const remp_kv_shape& sh = plan->shape;
+    if (t.num_seqs != plan->num_seqs)
+        return fail(REMP_E_INVALID, "new tables describe a different number of sequences");
+    if (t.num_seqs > 0 && (!t.seq_lens || !t.row_offsets)) return fail(REMP_E_INVALID, "new table arrays are NULL");
+    if (t.num_blocks < 0 || t.num_blocks > INT32_MAX) return fail(REMP_E_INVALID, "new num_blocks out of range");
+    if (plan->new_live_blocks > t.num_blocks)
+        return fail(REMP_E_CAPACITY, "the live cache needs " + std::to_string(plan->new_live_blocks) +
+                                         " blocks, the new pool has " + std::to_string(t.num_blocks));
+    if (dst->num_blocks < t.num_blocks) return fail(REMP_E_SIZE, "destination pool smaller than its tables");
+    int64_t nnz = 0;
+    if (t.num_seqs > 0) {
+        if (t.row_offsets[0] < 0) return fail(REMP_E_INVALID, "new row_offsets[0] < 0");
+        nnz = t.row_offsets[t.num_seqs];
+        if (nnz > 0 && !t.block_ids) return fail(REMP_E_INVALID, "new block_ids is NULL");
+    }
+    std::vector<uint8_t> used(static_cast<size_t>(t.num_blocks), 0);
+    for (int32_t q = 0; q < t.num_seqs; ++q) {
+        if (t.seq_lens[q] != plan->seq_lens[q])
+            return fail(REMP_E_INVALID, "new tables give sequence " + std::to_string(q) + " length " +
+                                            std::to_string(t.seq_lens[q]) + ", planned " +
+                                            std::to_string(plan->seq_lens[q]));
+        const int32_t a = t.row_offsets[q], b = t.row_offsets[q + 1];
+        if (b < a) return fail(REMP_E_INVALID, "new row_offsets decrease at sequence " + std::to_string(q));
+        const int64_t need = ceil_div(t.seq_lens[q], sh.new_block_size);
+        if (b - a < need) return fail(REMP_E_INVALID, "new table row of sequence " + std::to_string(q) + " too short");
+        for (int64_t j = 0; j < need; ++j) {
+            const int32_t id = t.block_ids[a + j];
+            if (id < 0 || id >= t.num_blocks)
+                return fail(REMP_E_RANGE, "new block id " + std::to_string(id) + " outside [0, " +
+                                              std::to_string(t.num_blocks) + ")");
+            if (used[id]) return fail(REMP_E_INVALID, "new block id " + std::to_string(id) + " used twice");
+            used[id] = 1;
+        }
+    }
+    *nnz_out = nnz;
+    return REMP_OK;
+}
+
 // Slices of the window for one side; fills `out`.  `pack`: items of old rank
-// `rank`; else items of new rank `rank`.
+// `rank`; else items of new rank `rank`.  skip_local leaves out the slices
+// whose peer is the same global rank.
 static remp_status collect_slices(const remp_kv_plan_t& p, bool pack, int32_t rank, int32_t l0, int32_t l1,
-                                  const remp_kv_pool& pool, const remp_buffer* staging,
+                                  const remp_kv_pool& pool, const remp_buffer* staging, bool skip_local,
                                   std::vector<HostSlice>& out) {
     const Ownership& mine = pack ? p.own_old : p.own_new;
     const int64_t hrow = static_cast<int64_t>(p.shape.head_dim) * p.shape.elem_bytes;
     const int32_t eb = p.shape.elem_bytes;
     for (const Item& it : p.items) {
         if ((pack ? it.src : it.dst) != rank || it.layer < l0 || it.layer >= l1) continue;
-        const Pair& pr = p.pairs[it.pair];
         const int32_t peer = pack ? it.dst : it.src;
+        if (skip_local && peer == rank) continue;
+        const Pair& pr = p.pairs[it.pair];
         const int32_t ws0 = std::max(l0, pr.layer_begin), ws1 = std::min(l1, pr.layer_end);
         const remp_buffer& sb = staging[peer];
         const int64_t need = static_cast<int64_t>(ws1 - ws0) * pr.slice_bytes;
@@ -477,6 +648,106 @@ static remp_status collect_slices(const remp_kv_plan_t& p, bool pack, int32_t ra
     return REMP_OK;
 }
 
+// ---------------------------------------------------------------------------
+// local copy: old pool -> new pool for slices that stay on the same rank
+// ---------------------------------------------------------------------------
+
+struct HostLocal {
+    uint64_t src_k, src_v, dst_k, dst_v;
+    uint32_t row_bytes;
+};
+
+template <int VEC>
+static remp_status launch_local_vec(const LocalArgs& a, dim3 grid, bool small, hipStream_t stream) {
+    if (small)
+        hipLaunchKernelGGL((copy_local<VEC, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((copy_local<VEC, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0, stream, a);
+    return hip_check(hipGetLastError(), "copy_local launch");
+}
+
+static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostLocal>& items, const char* ws,
+                                hipStream_t stream) {
+    const remp_kv_shape& sh = p.shape;
+    const WorkspaceLayout L = workspace_layout(p);
+    const int64_t n_desc = p.new_live_blocks;
+    if (items.empty() || n_desc == 0) return REMP_OK;
+    if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
+    const int64_t hrow = static_cast<int64_t>(sh.head_dim) * sh.elem_bytes;
+    const int64_t orow = p.own_old.heads_per_rank() * hrow, nrow = p.own_new.heads_per_rank() * hrow;
+    const int32_t bo = sh.old_block_size, bn = sh.new_block_size;
+    uint64_t bits = static_cast<uint64_t>(orow) | static_cast<uint64_t>(nrow) | 16u;
+    uint32_t max_row = 0;
+    for (const HostLocal& it : items) {
+        bits |= it.src_k | it.src_v | it.dst_k | it.dst_v | it.row_bytes;
+        max_row = std::max(max_row, it.row_bytes);
+    }
+    const int vec = static_cast<int>(bits & (~bits + 1));
+    const int64_t per_unit = static_cast<int64_t>(bn) * max_row;
+    const bool small = per_unit <= kSmallUnitBytes;
+    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kSmallWgBytes : kLargeWgBytes));
+    int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
+    C = std::min<int32_t>(C, std::max<int32_t>(1, kMaxLocalRows / bn));
+    if (bn > kMaxLocalRows) return fail(REMP_E_UNSUPPORTED, "new block size above the local-copy row limit");
+    if (static_cast<uint64_t>(C) * bn * (max_row / vec) >= (uint64_t(1) << 32))
+        return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^32 vectors");
+
+    LocalArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.new_desc = reinterpret_cast<const BlockDesc*>(ws + L.desc_new);
+    a.old_desc = reinterpret_cast<const BlockDesc*>(ws + L.desc_old);
+    a.tok_off = reinterpret_cast<const int32_t*>(ws + L.scan_new);
+    a.old_blk_off = reinterpret_cast<const int32_t*>(ws + L.scan_old) + (p.num_seqs + 1);
+    a.flag = reinterpret_cast<int32_t*>(const_cast<char*>(ws));
+    a.old_block_stride = orow * bo;
+    a.new_block_stride = nrow * bn;
+    a.n_new_desc = static_cast<int32_t>(n_desc);
+    a.n_old_desc = static_cast<int32_t>(p.old_live_blocks);
+    a.units_per_wg = C;
+    a.old_row_stride = static_cast<int32_t>(orow);
+    a.new_row_stride = static_cast<int32_t>(nrow);
+    a.old_block_size = bo;
+    a.new_block_size = bn;
+    const int64_t gx = (2 * n_desc + C - 1) / C;
+    if (g_trace_start) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
+    }
+    for (size_t first = 0; first < items.size(); first += kMaxLocalItems) {
+        const size_t cnt = std::min<size_t>(kMaxLocalItems, items.size() - first);
+        for (size_t i = 0; i < cnt; ++i) {
+            const HostLocal& h = items[first + i];
+            LocalItem& c = a.items[i];
+            c.src_k = h.src_k;
+            c.src_v = h.src_v;
+            c.dst_k = h.dst_k;
+            c.dst_v = h.dst_v;
+            c.row_bytes = h.row_bytes;
+            const FastDiv fv = make_fastdiv(h.row_bytes / vec);
+            const FastDiv fu = make_fastdiv(static_cast<uint32_t>(bn) * (h.row_bytes / vec));
+            c.vpr_magic = fv.magic;
+            c.vpr_shift = static_cast<uint16_t>(fv.shift);
+            c.unit_magic = fu.magic;
+            c.unit_shift = static_cast<uint16_t>(fu.shift);
+        }
+        const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
+        remp_status st;
+        switch (vec) {
+            case 16: st = launch_local_vec<16>(a, grid, small, stream); break;
+            case 8: st = launch_local_vec<8>(a, grid, small, stream); break;
+            case 4: st = launch_local_vec<4>(a, grid, small, stream); break;
+            case 2: st = launch_local_vec<2>(a, grid, small, stream); break;
+            default: st = launch_local_vec<1>(a, grid, small, stream); break;
+        }
+        if (st) return st;
+    }
+    if (g_trace_stop) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_stop, stream), "trace stop event")) return st;
+    }
+    return REMP_OK;
+}
+
+static bool ranges_overlap(uint64_t a, uint64_t an, uint64_t b, uint64_t bn) { return a < b + bn && b < a + an; }
+
 }  // namespace remp
 
 using namespace remp;
@@ -490,102 +761,131 @@ void remp_kv_set_trace_events(hipEvent_t start, hipEvent_t stop) {
 
 remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t layer_begin, int32_t layer_end,
                          const remp_kv_pool* src, const remp_dev_tables* old_tables, const remp_buffer* staging,
-                         void* workspace, int64_t workspace_bytes_, hipStream_t stream) {
+                         void* workspace, int64_t workspace_bytes_, uint32_t flags, hipStream_t stream) {
     clear_error();
     if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL)) return fail(REMP_E_INVALID, "unknown flags");
     if (old_rank < 0 || old_rank >= plan->own_old.world())
         return fail(REMP_E_RANGE, "old_rank " + std::to_string(old_rank) + " outside [0, " +
                                       std::to_string(plan->own_old.world()) + ")");
-    if (remp_status st = check_common(plan, layer_begin, layer_end, src, staging, workspace, workspace_bytes_,
-                                      plan->own_old.layers_per_stage()))
-        return st;
+    if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
+    if (remp_status st = check_pool(src, plan->own_old.layers_per_stage(), "source")) return st;
+    if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
+    if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     if (src->num_blocks < plan->old_num_blocks)
         return fail(REMP_E_SIZE, "source pool has fewer blocks than the old tables address");
-    if (!old_tables) return fail(REMP_E_INVALID, "device old tables are NULL");
-    if (plan->num_seqs > 0 && (!old_tables->seq_lens || !old_tables->row_offsets))
-        return fail(REMP_E_INVALID, "device old table arrays are NULL");
-    if (plan->old_nnz > 0 && !old_tables->block_ids) return fail(REMP_E_INVALID, "device old block ids are NULL");
+    if (remp_status st = check_dev_tables(plan, old_tables, plan->old_nnz, "old")) return st;
 
     std::vector<HostSlice> slices;
-    if (remp_status st = collect_slices(*plan, true, old_rank, layer_begin, layer_end, *src, staging, slices))
+    if (remp_status st = collect_slices(*plan, true, old_rank, layer_begin, layer_end, *src, staging,
+                                        (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
         return st;
     if (slices.empty() || plan->old_live_blocks == 0) return REMP_OK;
     const remp_kv_shape& sh = plan->shape;
     const int64_t row_stride = static_cast<int64_t>(plan->own_old.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
+    const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
     if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz, plan->old_num_blocks,
-                                       plan->old_live_blocks, ws, stream))
+                                       plan->old_live_blocks, ws, L.scan_old, L.desc_old, true, stream))
         return st;
     return launch_copy<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size, row_stride * sh.old_block_size,
-                             static_cast<int32_t>(row_stride), ws, stream);
+                             static_cast<int32_t>(row_stride), ws, L.desc_old, stream);
 }
 
 remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t layer_begin, int32_t layer_end,
                            const remp_buffer* staging, const remp_kv_pool* dst, const remp_block_tables* new_tables,
                            const remp_dev_tables* new_dev_tables, void* workspace, int64_t workspace_bytes_,
-                           hipStream_t stream) {
+                           uint32_t flags, hipStream_t stream) {
     clear_error();
     if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL)) return fail(REMP_E_INVALID, "unknown flags");
     if (new_rank < 0 || new_rank >= plan->own_new.world())
         return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
                                       std::to_string(plan->own_new.world()) + ")");
-    if (remp_status st = check_common(plan, layer_begin, layer_end, dst, staging, workspace, workspace_bytes_,
-                                      plan->own_new.layers_per_stage()))
-        return st;
-    // --- new tables: same population, valid rows, ids in range and used once
-    if (!new_tables) return fail(REMP_E_INVALID, "new tables are NULL");
-    const remp_block_tables& t = *new_tables;
-    const remp_kv_shape& sh = plan->shape;
-    if (t.num_seqs != plan->num_seqs) return fail(REMP_E_INVALID, "new tables describe a different number of sequences");
-    if (t.num_seqs > 0 && (!t.seq_lens || !t.row_offsets)) return fail(REMP_E_INVALID, "new table arrays are NULL");
-    if (t.num_blocks < 0 || t.num_blocks > INT32_MAX) return fail(REMP_E_INVALID, "new num_blocks out of range");
-    if (plan->new_live_blocks > t.num_blocks)
-        return fail(REMP_E_CAPACITY, "the live cache needs " + std::to_string(plan->new_live_blocks) +
-                                         " blocks, the new pool has " + std::to_string(t.num_blocks));
-    if (dst->num_blocks < t.num_blocks) return fail(REMP_E_SIZE, "destination pool smaller than its tables");
+    if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
+    if (remp_status st = check_pool(dst, plan->own_new.layers_per_stage(), "destination")) return st;
+    if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
+    if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     int64_t nnz = 0;
-    if (t.num_seqs > 0) {
-        if (t.row_offsets[0] < 0) return fail(REMP_E_INVALID, "new row_offsets[0] < 0");
-        nnz = t.row_offsets[t.num_seqs];
-        if (nnz > 0 && !t.block_ids) return fail(REMP_E_INVALID, "new block_ids is NULL");
-    }
-    {
-        std::vector<uint8_t> used(static_cast<size_t>(t.num_blocks), 0);
-        for (int32_t q = 0; q < t.num_seqs; ++q) {
-            if (t.seq_lens[q] != plan->seq_lens[q])
-                return fail(REMP_E_INVALID, "new tables give sequence " + std::to_string(q) + " length " +
-                                                std::to_string(t.seq_lens[q]) + ", planned " +
-                                                std::to_string(plan->seq_lens[q]));
-            const int32_t a = t.row_offsets[q], b = t.row_offsets[q + 1];
-            if (b < a) return fail(REMP_E_INVALID, "new row_offsets decrease at sequence " + std::to_string(q));
-            const int64_t need = ceil_div(t.seq_lens[q], sh.new_block_size);
-            if (b - a < need) return fail(REMP_E_INVALID, "new table row of sequence " + std::to_string(q) + " too short");
-            for (int64_t j = 0; j < need; ++j) {
-                const int32_t id = t.block_ids[a + j];
-                if (id < 0 || id >= t.num_blocks)
-                    return fail(REMP_E_RANGE, "new block id " + std::to_string(id) + " outside [0, " +
-                                                  std::to_string(t.num_blocks) + ")");
-                if (used[id]) return fail(REMP_E_INVALID, "new block id " + std::to_string(id) + " used twice");
-                used[id] = 1;
-            }
-        }
-    }
-    if (!new_dev_tables) return fail(REMP_E_INVALID, "device new tables are NULL");
-    if (plan->num_seqs > 0 && (!new_dev_tables->seq_lens || !new_dev_tables->row_offsets))
-        return fail(REMP_E_INVALID, "device new table arrays are NULL");
-    if (nnz > 0 && !new_dev_tables->block_ids) return fail(REMP_E_INVALID, "device new block ids are NULL");
+    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz)) return st;
+    if (remp_status st = check_dev_tables(plan, new_dev_tables, nnz, "new")) return st;
 
     std::vector<HostSlice> slices;
-    if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging, slices))
+    if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging,
+                                        (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
         return st;
     if (slices.empty() || plan->new_live_blocks == 0) return REMP_OK;
+    const remp_kv_shape& sh = plan->shape;
     const int64_t row_stride = static_cast<int64_t>(plan->own_new.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
+    const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
-    if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, t.num_blocks,
-                                       plan->new_live_blocks, ws, stream))
+    if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
+                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream))
         return st;
     return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
-                              static_cast<int32_t>(row_stride), ws, stream);
+                              static_cast<int32_t>(row_stride), ws, L.desc_new, stream);
+}
+
+remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t layer_begin, int32_t layer_end,
+                               const remp_kv_pool* src, const remp_dev_tables* old_tables, const remp_kv_pool* dst,
+                               const remp_block_tables* new_tables, const remp_dev_tables* new_dev_tables,
+                               void* workspace, int64_t workspace_bytes_, hipStream_t stream) {
+    clear_error();
+    if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (rank < 0 || rank >= plan->own_old.world() || rank >= plan->own_new.world())
+        return fail(REMP_E_RANGE, "rank " + std::to_string(rank) + " is not a rank of both topologies");
+    if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
+    if (remp_status st = check_pool(src, plan->own_old.layers_per_stage(), "source")) return st;
+    if (remp_status st = check_pool(dst, plan->own_new.layers_per_stage(), "destination")) return st;
+    if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
+    if (src->num_blocks < plan->old_num_blocks)
+        return fail(REMP_E_SIZE, "source pool has fewer blocks than the old tables address");
+    if (remp_status st = check_dev_tables(plan, old_tables, plan->old_nnz, "old")) return st;
+    int64_t nnz = 0;
+    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz)) return st;
+    if (remp_status st = check_dev_tables(plan, new_dev_tables, nnz, "new")) return st;
+
+    const remp_kv_shape& sh = plan->shape;
+    const int64_t hrow = static_cast<int64_t>(sh.head_dim) * sh.elem_bytes;
+    const int64_t old_layer_bytes = plan->own_old.heads_per_rank() * hrow * sh.old_block_size * src->num_blocks;
+    const int64_t new_layer_bytes = plan->own_new.heads_per_rank() * hrow * sh.new_block_size * dst->num_blocks;
+    const int32_t eb = sh.elem_bytes;
+    std::vector<HostLocal> items;
+    for (const Item& it : plan->items) {
+        if (it.src != rank || it.dst != rank || it.layer < layer_begin || it.layer >= layer_end) continue;
+        const int32_t lo = it.layer - plan->own_old.first_layer(rank), ln = it.layer - plan->own_new.first_layer(rank);
+        void* sk = src->k[lo];
+        void* sv = src->v[lo];
+        void* dk = dst->k[ln];
+        void* dv = dst->v[ln];
+        if (!sk || !sv || !dk || !dv)
+            return fail(REMP_E_INVALID, "pool storage of layer " + std::to_string(it.layer) + " is NULL");
+        if (!aligned(sk, eb) || !aligned(sv, eb) || !aligned(dk, eb) || !aligned(dv, eb))
+            return fail(REMP_E_ALIGN, "pool storage not element aligned");
+        const uint64_t s2[2] = {reinterpret_cast<uint64_t>(sk), reinterpret_cast<uint64_t>(sv)};
+        const uint64_t d2[2] = {reinterpret_cast<uint64_t>(dk), reinterpret_cast<uint64_t>(dv)};
+        for (uint64_t a : s2)
+            for (uint64_t b : d2)
+                if (ranges_overlap(a, old_layer_bytes, b, new_layer_bytes))
+                    return fail(REMP_E_INVALID, "old and new storage of layer " + std::to_string(it.layer) + " overlap");
+        HostLocal h;
+        h.src_k = s2[0] + static_cast<uint64_t>(it.head_begin - plan->own_old.first_head(rank)) * hrow;
+        h.src_v = s2[1] + static_cast<uint64_t>(it.head_begin - plan->own_old.first_head(rank)) * hrow;
+        h.dst_k = d2[0] + static_cast<uint64_t>(it.head_begin - plan->own_new.first_head(rank)) * hrow;
+        h.dst_v = d2[1] + static_cast<uint64_t>(it.head_begin - plan->own_new.first_head(rank)) * hrow;
+        h.row_bytes = static_cast<uint32_t>(it.head_count * hrow);
+        items.push_back(h);
+    }
+    if (items.empty() || plan->new_live_blocks == 0) return REMP_OK;
+    const WorkspaceLayout L = workspace_layout(*plan);
+    char* ws = static_cast<char*>(workspace);
+    if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz, plan->old_num_blocks,
+                                       plan->old_live_blocks, ws, L.scan_old, L.desc_old, true, stream))
+        return st;
+    if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
+                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, false, stream))
+        return st;
+    return launch_local(*plan, items, ws, stream);
 }
 
 }  // extern "C"

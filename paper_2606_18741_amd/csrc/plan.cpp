@@ -33,16 +33,21 @@ const Pair* find_pair(const remp_kv_plan_t& p, int32_t src, int32_t dst) {
     return i < 0 ? nullptr : &p.pairs[i];
 }
 
-// Workspace: [flag:4][pad][tok_off: S+1][blk_off: S+1] then, 256-aligned, block descriptors.
-int64_t workspace_desc_offset(const remp_kv_plan_t& p) {
-    int64_t head = 256 + 2 * (static_cast<int64_t>(p.num_seqs) + 1) * 4;
-    return (head + 255) / 256 * 256;
+static int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
+
+// Workspace: [mismatch flag, 256 B][old scan][new scan][old descriptors][new descriptors], 256-aligned.
+WorkspaceLayout workspace_layout(const remp_kv_plan_t& p) {
+    WorkspaceLayout w;
+    const int64_t scan = align256(2 * (static_cast<int64_t>(p.num_seqs) + 1) * 4);
+    w.scan_old = 256;
+    w.scan_new = w.scan_old + scan;
+    w.desc_old = w.scan_new + scan;
+    w.desc_new = w.desc_old + align256(std::max<int64_t>(p.old_live_blocks, 1) * 16);
+    w.total = w.desc_new + align256(std::max<int64_t>(p.new_live_blocks, 1) * 16);
+    return w;
 }
 
-int64_t workspace_bytes(const remp_kv_plan_t& p) {
-    int64_t n = std::max(p.old_live_blocks, p.new_live_blocks);
-    return workspace_desc_offset(p) + std::max<int64_t>(n, 1) * 16;
-}
+int64_t workspace_bytes(const remp_kv_plan_t& p) { return workspace_layout(p).total; }
 
 static remp_status check_topo(const remp_topo* t, const char* which, const remp_kv_shape& s) {
     if (!t) return fail(REMP_E_INVALID, std::string(which) + " topology is NULL");

@@ -64,8 +64,16 @@ remp_status fail(remp_status st, const std::string& msg);
 void clear_error();
 
 int64_t ceil_div(int64_t a, int64_t b);
+
+// Byte offsets inside the caller's workspace.  Each scan area holds token and
+// block offsets per sequence ([S+1] int32 each); each descriptor area holds
+// one 16-byte descriptor per live block.  Pack uses the old areas, unpack the
+// new ones, the local copy both.
+struct WorkspaceLayout {
+    int64_t scan_old, scan_new, desc_old, desc_new, total;
+};
+WorkspaceLayout workspace_layout(const remp_kv_plan_t& p);
 int64_t workspace_bytes(const remp_kv_plan_t& p);
-int64_t workspace_desc_offset(const remp_kv_plan_t& p);
 const Pair* find_pair(const remp_kv_plan_t& p, int32_t src, int32_t dst);
 
 }  // namespace remp

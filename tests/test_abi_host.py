@@ -255,13 +255,13 @@ def test_pack_validation_errors():
     s = _setup()
     p, L = s["p"], s["L"]
     ok = dict(old_rank=0, src=s["src"], old_dev_tables=s["dev"], staging=rk.buffers(s["out0"]),
-              workspace=s["ws"], workspace_bytes=s["ws_bytes"], stream=0, layer_begin=0, layer_end=L)
+              workspace=s["ws"], workspace_bytes=s["ws_bytes"], stream=0, layer_begin=0, layer_end=L, flags=0)
 
     def call(**kw):
         a = dict(ok)
         a.update(kw)
         rk.remp_kv_pack(p.handle, a["old_rank"], a["layer_begin"], a["layer_end"], a["src"], a["old_dev_tables"],
-                        a["staging"], a["workspace"], a["workspace_bytes"], a["stream"])
+                        a["staging"], a["workspace"], a["workspace_bytes"], a["flags"], a["stream"])
 
     _expect("REMP_E_RANGE", call, old_rank=2)
     _expect("REMP_E_RANGE", call, old_rank=-1)
@@ -290,8 +290,13 @@ def test_pack_validation_errors():
     ks = list(s["src"]._k)
     ks[0] = ks[0] + 1
     _expect("REMP_E_ALIGN", call, src=rk.PoolArg(ks, list(s["src"]._v), 64))
+    _expect("REMP_E_INVALID", call, flags=2)
+    # with REMP_KV_SKIP_LOCAL the local pair's staging entry may be absent
+    local_null = list(s["out0"])
+    local_null[0] = None
+    _expect("REMP_E_INVALID", call, staging=rk.buffers(local_null), layer_begin=0, layer_end=1)
     lib = rk.load()
-    assert lib.remp_kv_pack(None, 0, 0, 1, None, None, None, None, 0, None) == -1
+    assert lib.remp_kv_pack(None, 0, 0, 1, None, None, None, None, 0, 0, None) == -1
     # an empty window is valid and enqueues nothing
     call(layer_begin=2, layer_end=2)
 
@@ -301,13 +306,13 @@ def test_unpack_validation_errors():
     s = _setup()
     p, L, nt = s["p"], s["L"], s["new_t"]
     ok = dict(new_rank=0, staging=rk.buffers(s["in0"]), dst=s["dst"], tables=rk.HostTables.of(nt),
-              dev=s["dev"], workspace=s["ws"], workspace_bytes=s["ws_bytes"], layer_begin=0, layer_end=L)
+              dev=s["dev"], workspace=s["ws"], workspace_bytes=s["ws_bytes"], layer_begin=0, layer_end=L, flags=0)
 
     def call(**kw):
         a = dict(ok)
         a.update(kw)
         rk.remp_kv_unpack(p.handle, a["new_rank"], a["layer_begin"], a["layer_end"], a["staging"], a["dst"],
-                          a["tables"], a["dev"], a["workspace"], a["workspace_bytes"], 0)
+                          a["tables"], a["dev"], a["workspace"], a["workspace_bytes"], a["flags"], 0)
 
     _expect("REMP_E_RANGE", call, new_rank=2)
     _expect("REMP_E_INVALID", call, tables=rk.HostTables(nt.seq_lens[:2], nt.offsets[:3], nt.ids, 64))
@@ -334,6 +339,36 @@ def test_unpack_validation_errors():
     if int(nt.seq_lens[0]) > 0:
         _expect("REMP_E_INVALID", call, tables=rk.HostTables.of(short))
     call(layer_begin=0, layer_end=0)
+    _expect("REMP_E_INVALID", call, flags=8)
+
+
+@cpu_only
+def test_copy_local_validation_errors():
+    s = _setup()
+    p, L, nt = s["p"], s["L"], s["new_t"]
+    ok = dict(rank=0, src=s["src"], odev=s["dev"], dst=s["dst"], tables=rk.HostTables.of(nt), ndev=s["dev"],
+              workspace=s["ws"], workspace_bytes=s["ws_bytes"], layer_begin=0, layer_end=L)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        rk.remp_kv_copy_local(p.handle, a["rank"], a["layer_begin"], a["layer_end"], a["src"], a["odev"], a["dst"],
+                              a["tables"], a["ndev"], a["workspace"], a["workspace_bytes"], 0)
+
+    _expect("REMP_E_RANGE", call, rank=2)
+    _expect("REMP_E_RANGE", call, layer_end=L + 1)
+    _expect("REMP_E_INVALID", call, src=None)
+    _expect("REMP_E_INVALID", call, dst=s["src"])                   # wrong layer count for the new topology
+    _expect("REMP_E_ALIGN", call, workspace=s["ws"] + 4)
+    ids = nt.ids.copy()
+    ids[1] = ids[0]
+    _expect("REMP_E_INVALID", call, tables=rk.HostTables(nt.seq_lens, nt.offsets, ids, 64))
+    _expect("REMP_E_INVALID", call, odev=rk.dev_tables(0, 0, 0))
+    # old and new storage of a layer overlapping is refused
+    ks = list(s["dst"]._k)
+    ks[0] = s["src"]._k[0]
+    _expect("REMP_E_INVALID", call, dst=rk.PoolArg(ks, list(s["dst"]._v), 64))
+    call(layer_begin=1, layer_end=1)                                 # empty window: nothing to do
 
 
 def test_one_hip_runtime_in_process():

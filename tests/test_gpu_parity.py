@@ -34,8 +34,12 @@ def _rk():
     return rk
 
 
-def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None):
-    """Pack every old rank, unpack every new rank, per layer window.  Returns device state."""
+def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None, local=False):
+    """Pack every old rank, unpack every new rank, per layer window.  Returns device state.
+
+    local: pack and unpack skip the slices a rank keeps, and remp_kv_copy_local
+    moves those pool to pool.
+    """
     rk = _rk()
     L = w.num_layers
     plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(old_tables))
@@ -45,32 +49,40 @@ def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None):
            for r in range(W_old)}
     dst = {q: RankPool.from_host(new_host[q], rank_layers(q, w.new_topo, L), new_tables.num_blocks, q)
            for q in range(W_new)}
-    pairs = [(p.src, p.dst) for p in plan.pairs]
+    pairs = [(p.src, p.dst) for p in plan.pairs if not (local and p.src == p.dst)]
     staging = staging_for_pairs(plan, w.seed, pairs)
     ws = Workspace(plan)
     stream = stream_handle()
     flags = []
+    fl = rk.REMP_KV_SKIP_LOCAL if local else 0
     for (l0, l1) in (windows or [(0, L)]):
         for r in range(W_old):
             plan.pack(r, src[r].arg, dto.dev, window_args(plan, staging, r, W_new, True, l0, l1),
-                      ws.buf, ws.bytes, stream, l0, l1)
+                      ws.buf, ws.bytes, stream, l0, l1, flags=fl)
         torch.cuda.synchronize()
         flags.append(ws.flag())
         for q in range(W_new):
             plan.unpack(q, window_args(plan, staging, q, W_old, False, l0, l1), dst[q].arg, dtn.host, dtn.dev,
-                        ws.buf, ws.bytes, stream, l0, l1)
+                        ws.buf, ws.bytes, stream, l0, l1, flags=fl)
         torch.cuda.synchronize()
         flags.append(ws.flag())
+        if local:
+            for r in range(min(W_old, W_new)):
+                plan.copy_local(r, src[r].arg, dto.dev, dst[r].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream,
+                                l0, l1)
+            torch.cuda.synchronize()
+            flags.append(ws.flag())
     return plan, src, dst, staging, flags
 
 
-def check_against_oracle(w, inp, windows=None, log_name=""):
+def check_against_oracle(w, inp, windows=None, log_name="", local=False):
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables)
     new_host = hostpools.sentinel_pools(w, inp.new_tables)
-    log(f"[parity] {log_name or w.name}: T={int(inp.lens.sum())} windows={windows}")
-    plan, src, dst, staging, flags = migrate_all(w, inp.old_tables, inp.new_tables, old_host, new_host, windows)
-    pairs = [(p.src, p.dst) for p in plan.pairs]
+    log(f"[parity] {log_name or w.name}: T={int(inp.lens.sum())} windows={windows} local={local}")
+    plan, src, dst, staging, flags = migrate_all(w, inp.old_tables, inp.new_tables, old_host, new_host, windows,
+                                                 local)
+    pairs = [(p.src, p.dst) for p in plan.pairs if not (local and p.src == p.dst)]
     st = oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables,
                         inp.new_tables, pairs=pairs)
     assert all(f == 0 for f in flags), flags
@@ -242,3 +254,25 @@ def test_mismatched_device_tables_are_contained():
     assert ws.flag() != 0
     for p in pairs:                        # nothing was copied
         assert torch.equal(staging[p], before[p])
+
+
+# ---------------------------------------------------------------------------
+# local fast path: slices a rank keeps move pool to pool, the rest through staging
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny", "mha7b", "mha13b", "gqa70b", "gqa70b_long"])
+def test_local_fast_path(name):
+    w = synthkv.WORKLOADS[name]
+    if name != "tiny":
+        w = synthkv.reduced(w, num_seqs=5, max_len=300)
+    check_against_oracle(w, synthkv.make_inputs(w), local=True)
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_local_fast_path_edge_case(name):
+    check_against_oracle(EDGE[name], synthkv.make_inputs(EDGE[name]), log_name=name, local=True)
+
+
+def test_local_fast_path_windows():
+    w = synthkv.reduced(synthkv.GQA_70B, num_seqs=3, max_len=200)
+    check_against_oracle(w, synthkv.make_inputs(w), windows=[(0, 13), (13, 40), (40, 80)], local=True)

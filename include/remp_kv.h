@@ -21,7 +21,12 @@
  * Conventions (readings of points the paper leaves open):
  *   - ranks:  rank(pp, tp) = pp * TP + tp;
  *   - layers: stage p of PP holds layers [p*L/PP, (p+1)*L/PP);  L % PP == 0;
- *   - heads:  tensor rank t of TP holds KV heads [t*H/TP, (t+1)*H/TP); H % TP == 0;
+ *   - heads:  with TP <= H (H % TP == 0) tensor rank t holds KV heads
+ *             [t*H/TP, (t+1)*H/TP); with TP > H (TP % H == 0, GQA replication)
+ *             it holds the single head t*H/TP, so each head has TP/H replicas;
+ *             a replicated head is taken from the destination itself if it
+ *             holds a replica, else from old replica (its index among the
+ *             head's new holders) mod (number of old replicas);
  *   - paged storage, per local layer, K and V separately:
  *       [num_blocks][block_size][H/TP][head_dim] elements of elem_bytes bytes,
  *     row-major; token t of sequence s lives in block ids[row_offsets[s] + t / block_size],
@@ -57,7 +62,8 @@ extern "C" {
 typedef enum {
     REMP_OK = 0,
     REMP_E_INVALID = -1,     /* malformed argument: null pointer, inconsistent tables, duplicate block id */
-    REMP_E_UNSUPPORTED = -2, /* valid request this version does not handle: H % TP != 0, L % PP != 0 */
+    REMP_E_UNSUPPORTED = -2, /* valid request this version does not handle: L % PP != 0, or TP neither
+                                divides nor is a multiple of the KV head count */
     REMP_E_RANGE = -3,       /* rank, layer window or block id out of range */
     REMP_E_CAPACITY = -4,    /* the new pool cannot hold the live cache (Section 3.4.5, capacity) */
     REMP_E_ALIGN = -5,       /* a device pointer is not aligned to the element size */

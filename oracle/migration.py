@@ -7,26 +7,33 @@ HIP library or its Python binding and imports neither.
 What it computes is the plain definition the migration has to reach
 (Section 3.4.1, logical KV cache model): element KV[l, b, h] held by
 rank(l, h, T_old) must end up, unchanged, on rank(l, h, T_new).  The oracle
-does not run the paper's plan construction (Algorithm 1); it materialises the
-logical slice of each (sequence, layer) from the old shards and writes it into
-the new shards, one slice at a time, in NumPy.
+does not run the paper's plan construction (Algorithm 1); for every
+(sequence, layer) it reads each head a new rank needs from the old rank that
+supplies it and writes it into the new shard, in NumPy.
 
 Readings of points the paper leaves open (each one is listed in the design doc):
 
-* ownership: pp_owner(l, PP) = l // (L / PP) (equal contiguous layer ranges),
-  tp_owner(h, TP) = h // (H / TP) (equal contiguous head ranges) and
-  rank(pp, tp) = pp * TP + tp;  L % PP == 0 and H % TP == 0 are required;
+* ownership: pp_owner(l, PP) = l // (L / PP) (equal contiguous layer ranges)
+  and rank(pp, tp) = pp * TP + tp, L % PP == 0; heads: with TP <= H
+  (H % TP == 0) tensor rank t holds [t*H/TP, (t+1)*H/TP); with TP > H
+  (TP % H == 0, GQA replication, allowed by the head-coverage invariant of
+  Section 3.4.5) it holds the single head t*H/TP, so each head has TP/H
+  replicas;
+* source of a head when the old topology replicates it: the destination rank
+  itself if it holds a replica (a local copy), else the old replica whose
+  index among the head's old replicas is (destination's index among the
+  head's new holders) mod (number of old replicas);
 * paged storage of a rank: per global layer it owns, K and V arrays of shape
-  [num_blocks, block_size, H / TP, head_dim]; token t of sequence s sits in
-  block table[s][t // block_size], slot t % block_size; only live tokens
-  (t < n_s) are payload;
+  [num_blocks, block_size, heads it holds, head_dim]; token t of sequence s
+  sits in block table[s][t // block_size], slot t % block_size; only live
+  tokens (t < n_s) are payload;
 * the block mapping across the switch is the caller's new block tables (the
   "deterministic block remapping" of Section 3.4.5); the new block size may
   differ from the old one;
 * K and V are two arrays moved identically;
 * staging, the contiguous buffer an old rank r fills for a new rank q: the
   (r, q) slices in ascending layer order, each slice laid out as
-  [kv][token of all sequences, sequence-major][head in the overlap][head_dim].
+  [kv][token of all sequences, sequence-major][head of the pair][head_dim].
 
 Array conventions used throughout:
 * pools: {rank: {global layer: ndarray [2, num_blocks, block_size, H_loc, D]}}
@@ -43,7 +50,7 @@ import numpy as np
 
 
 # ---------------------------------------------------------------------------
-# topology and ownership (Section 3.4.1)
+# topology and ownership (Section 3.4.1; replication: Section 3.4.5)
 # ---------------------------------------------------------------------------
 
 @dataclass(frozen=True)
@@ -59,8 +66,8 @@ class Topology:
 def check_divisible(topo: Topology, L: int, H: int) -> None:
     if topo.tp < 1 or topo.pp < 1:
         raise ValueError("TP and PP must be positive")
-    if L % topo.pp or H % topo.tp:
-        raise ValueError(f"(TP={topo.tp}, PP={topo.pp}) does not divide L={L}, H={H}")
+    if L % topo.pp or (H % topo.tp and topo.tp % H):
+        raise ValueError(f"(TP={topo.tp}, PP={topo.pp}) does not fit L={L}, H={H}")
 
 
 def pp_owner(l: int, topo: Topology, L: int) -> int:
@@ -68,9 +75,20 @@ def pp_owner(l: int, topo: Topology, L: int) -> int:
     return l // (L // topo.pp)
 
 
+def tp_owners(h: int, topo: Topology, H: int) -> List[int]:
+    """Tensor ranks that hold KV head h (one, or TP/H replicas)."""
+    if topo.tp <= H:
+        return [h // (H // topo.tp)]
+    rep = topo.tp // H
+    return list(range(h * rep, (h + 1) * rep))
+
+
 def tp_owner(h: int, topo: Topology, H: int) -> int:
-    """Tensor-parallel rank that holds KV head h."""
-    return h // (H // topo.tp)
+    """The tensor rank that holds KV head h (topologies without replication)."""
+    owners = tp_owners(h, topo, H)
+    if len(owners) != 1:
+        raise ValueError("head is replicated in this topology")
+    return owners[0]
 
 
 def rank_of(pp: int, tp: int, topo: Topology) -> int:
@@ -78,9 +96,23 @@ def rank_of(pp: int, tp: int, topo: Topology) -> int:
     return pp * topo.tp + tp
 
 
+def holders(l: int, h: int, topo: Topology, L: int, H: int) -> List[int]:
+    """Global ranks holding (layer l, head h): rank(l, h, T) of Section 3.4.1, as a set."""
+    return [rank_of(pp_owner(l, topo, L), t, topo) for t in tp_owners(h, topo, H)]
+
+
 def owner(l: int, h: int, topo: Topology, L: int, H: int) -> int:
-    """rank(l, h, T) of Section 3.4.1."""
+    """rank(l, h, T) for a topology without replication."""
     return rank_of(pp_owner(l, topo, L), tp_owner(h, topo, H), topo)
+
+
+def source_of(l: int, h: int, q: int, old: Topology, new: Topology, L: int, H: int) -> int:
+    """The old rank that supplies (layer l, head h) to new rank q."""
+    cands = holders(l, h, old, L, H)
+    if q in cands:
+        return q
+    news = holders(l, h, new, L, H)
+    return cands[news.index(q) % len(cands)]
 
 
 def stage_of_rank(r: int, topo: Topology) -> Tuple[int, int]:
@@ -95,6 +127,9 @@ def layers_of(r: int, topo: Topology, L: int) -> range:
 
 def heads_of(r: int, topo: Topology, H: int) -> range:
     _, t = stage_of_rank(r, topo)
+    if topo.tp > H:
+        h = t * H // topo.tp
+        return range(h, h + 1)
     per = H // topo.tp
     return range(t * per, (t + 1) * per)
 
@@ -102,17 +137,19 @@ def heads_of(r: int, topo: Topology, H: int) -> range:
 def pair_slices(old: Topology, new: Topology, L: int, H: int) -> Dict[Tuple[int, int], Tuple[List[int], List[int]]]:
     """For each (old rank r, new rank q) that exchanges data: (layers, heads).
 
-    By definition: group every (l, h) by (rank(l,h,T_old), rank(l,h,T_new)).
+    By definition: every (l, h) goes to each of its new holders q, from
+    source_of(l, h, q); group (l, h) by that (source, holder) pair.
     """
     check_divisible(old, L, H)
     check_divisible(new, L, H)
     groups: Dict[Tuple[int, int], Tuple[set, set]] = {}
     for l in range(L):
         for h in range(H):
-            key = (owner(l, h, old, L, H), owner(l, h, new, L, H))
-            ls, hs = groups.setdefault(key, (set(), set()))
-            ls.add(l)
-            hs.add(h)
+            for q in holders(l, h, new, L, H):
+                key = (source_of(l, h, q, old, new, L, H), q)
+                ls, hs = groups.setdefault(key, (set(), set()))
+                ls.add(l)
+                hs.add(h)
     return {k: (sorted(v[0]), sorted(v[1])) for k, v in sorted(groups.items())}
 
 
@@ -146,31 +183,13 @@ def token_offsets(seq_lens: np.ndarray) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
-# materialise and re-shard
+# re-shard
 # ---------------------------------------------------------------------------
 
-def materialise(old_pools, old: Topology, L: int, H: int, old_tables, s: int, l: int,
-                heads: Iterable[int]) -> np.ndarray:
-    """Logical slice X[kv, t, h, :] of sequence s at layer l from the old shards.
-
-    Heads not in `heads` are left zero (their old owner need not be present).
-    """
-    heads = sorted(set(heads))
-    blk, slot = token_slots(old_tables, s)
-    n = blk.shape[0]
-    D, dtype = None, None
-    X = None
-    for h in heads:
-        r = owner(l, h, old, L, H)
-        store = old_pools[r][l]                          # [2, nb, bs, H_loc, D]
-        if X is None:
-            D, dtype = store.shape[-1], store.dtype
-            X = np.zeros((2, n, H, D), dtype=dtype)
-        h_loc = h - heads_of(r, old, H).start
-        X[:, :, h, :] = store[:, blk, slot, h_loc, :]
-    if X is None:
-        raise ValueError("no heads requested")
-    return X
+def gather_rows(store: np.ndarray, tables, s: int) -> np.ndarray:
+    """Rows of sequence s from one rank's layer storage: [kv, token, local head, D]."""
+    blk, slot = token_slots(tables, s)
+    return store[:, blk, slot, :, :]
 
 
 def reshard(old_pools, new_pools, old: Topology, new: Topology, L: int, H: int,
@@ -178,14 +197,14 @@ def reshard(old_pools, new_pools, old: Topology, new: Topology, L: int, H: int,
             pairs: Optional[Iterable[Tuple[int, int]]] = None):
     """Re-shard the live KV cache from `old` to `new`.
 
-    old_pools: {old rank: {layer: [2, nb_o, bs_o, H/TP_o, D]}} -- read only.
-    new_pools: {new rank: {layer: [2, nb_n, bs_n, H/TP_n, D]}} -- written in
+    old_pools: {old rank: {layer: [2, nb_o, bs_o, H_loc, D]}} -- read only.
+    new_pools: {new rank: {layer: [2, nb_n, bs_n, H_loc', D]}} -- written in
                place at live slots only; ranks or layers absent are skipped.
     layers:    global layers to process (default: all).
     pairs:     (old rank, new rank) pairs whose staging to return (default: none).
 
-    Returns {(r, q): {layer: ndarray [2, T, |H_r & H_q|, D]}} for the requested
-    pairs and processed layers.
+    Returns {(r, q): {layer: ndarray [2, T, |heads of the pair|, D]}} for the
+    requested pairs and processed layers.
     """
     check_divisible(old, L, H)
     check_divisible(new, L, H)
@@ -197,38 +216,37 @@ def reshard(old_pools, new_pools, old: Topology, new: Topology, L: int, H: int,
     tok_off = token_offsets(old_tables.seq_lens)
     T = int(tok_off[-1])
     staging: Dict[Tuple[int, int], Dict[int, np.ndarray]] = {p: {} for p in pairs}
-
+    slices = pair_slices(old, new, L, H)
     any_store = next(iter(next(iter(old_pools.values())).values()))
     D, dtype = any_store.shape[-1], any_store.dtype
+
     for l in layers:
-        # heads this layer must supply: to present new ranks, and to requested staging
-        need = set()
-        targets = []
+        # (new rank q, head h) <- (old rank r, its local head) for present new ranks
+        moves = []
         for q, per_layer in new_pools.items():
             if l in per_layer and l in layers_of(q, new, L):
-                targets.append(q)
-                need.update(heads_of(q, new, H))
-        slices = []
+                for h in heads_of(q, new, H):
+                    r = source_of(l, h, q, old, new, L, H)
+                    moves.append((q, h - heads_of(q, new, H).start, r, h - heads_of(r, old, H).start))
+        cuts = []
         for (r, q) in pairs:
-            if l in layers_of(r, old, L) and l in layers_of(q, new, L):
-                hs = sorted(set(heads_of(r, old, H)) & set(heads_of(q, new, H)))
-                if hs:
-                    staging[(r, q)][l] = np.zeros((2, T, len(hs), D), dtype=dtype)
-                    slices.append(((r, q), hs))
-                    need.update(hs)
-        if not need:
+            if (r, q) in slices and l in slices[(r, q)][0]:
+                hs = slices[(r, q)][1]
+                staging[(r, q)][l] = np.zeros((2, T, len(hs), D), dtype=dtype)
+                cuts.append(((r, q), [h - heads_of(r, old, H).start for h in hs]))
+        sources = {m[2] for m in moves} | {k[0] for k, _ in cuts}
+        if not sources:
             continue
         for s in range(S):
             n = int(old_tables.seq_lens[s])
             if n == 0:
                 continue
-            X = materialise(old_pools, old, L, H, old_tables, s, l, need)
+            rows = {r: gather_rows(old_pools[r][l], old_tables, s) for r in sources}
             nblk, nslot = token_slots(new_tables, s)
-            for q in targets:
-                hr = heads_of(q, new, H)
-                new_pools[q][l][:, nblk, nslot, :, :] = X[:, :, hr.start:hr.stop, :]
-            for key, hs in slices:
-                staging[key][l][:, tok_off[s]:tok_off[s] + n, :, :] = X[:, :, hs, :]
+            for q, hq, r, hr in moves:
+                new_pools[q][l][:, nblk, nslot, hq, :] = rows[r][:, :, hr, :]
+            for key, hl in cuts:
+                staging[key][l][:, tok_off[s]:tok_off[s] + n, :, :] = rows[key[0]][:, :, hl, :]
     return staging
 
 
@@ -244,17 +262,22 @@ def staging_buffer(items: Dict[int, np.ndarray]) -> np.ndarray:
 # point queries (for checking sampled rows of very large migrations)
 # ---------------------------------------------------------------------------
 
-def old_location(l: int, h: int, s: int, t: int, old: Topology, L: int, H: int, old_tables):
-    """(old rank, block, slot, local head) holding token t of sequence s, layer l, head h."""
-    r = owner(l, h, old, L, H)
+def old_location(l: int, h: int, s: int, t: int, old: Topology, L: int, H: int, old_tables,
+                 new: Optional[Topology] = None, dst: Optional[int] = None):
+    """(old rank, block, slot, local head) holding token t of sequence s, layer l, head h.
+
+    With a replicating old topology the supplying replica depends on the
+    destination: pass new and dst.
+    """
+    r = holders(l, h, old, L, H)[0] if dst is None else source_of(l, h, dst, old, new, L, H)
     bs = int(old_tables.block_size)
     blk = int(old_tables.row(s)[t // bs])
     return r, blk, t % bs, h - heads_of(r, old, H).start
 
 
-def new_location(l: int, h: int, s: int, t: int, new: Topology, L: int, H: int, new_tables):
+def new_location(l: int, h: int, s: int, t: int, new: Topology, L: int, H: int, new_tables, replica: int = 0):
     """(new rank, block, slot, local head) that must hold the same element after the switch."""
-    q = owner(l, h, new, L, H)
+    q = holders(l, h, new, L, H)[replica]
     bs = int(new_tables.block_size)
     blk = int(new_tables.row(s)[t // bs])
     return q, blk, t % bs, h - heads_of(q, new, H).start

@@ -53,9 +53,10 @@ static remp_status check_topo(const remp_topo* t, const char* which, const remp_
     if (!t) return fail(REMP_E_INVALID, std::string(which) + " topology is NULL");
     if (t->tp < 1 || t->pp < 1)
         return fail(REMP_E_INVALID, std::string(which) + " topology needs TP >= 1 and PP >= 1");
-    if (s.num_kv_heads % t->tp != 0)
+    if (s.num_kv_heads % t->tp != 0 && t->tp % s.num_kv_heads != 0)
         return fail(REMP_E_UNSUPPORTED, std::string(which) + " TP=" + std::to_string(t->tp) +
-                                            " does not divide num_kv_heads=" + std::to_string(s.num_kv_heads));
+                                            " neither divides nor is a multiple of num_kv_heads=" +
+                                            std::to_string(s.num_kv_heads));
     if (s.num_layers % t->pp != 0)
         return fail(REMP_E_UNSUPPORTED, std::string(which) + " PP=" + std::to_string(t->pp) +
                                             " does not divide num_layers=" + std::to_string(s.num_layers));
@@ -158,7 +159,12 @@ remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo, c
     p->old_live_blocks = nb_old;
     p->new_live_blocks = nb_new;
 
-    // --- Algorithm 1: per layer, intersect target and source head ranges -----
+    // --- Algorithm 1: per layer, each new tensor rank's head range against the
+    // old tensor ranks' ranges; every non-empty overlap is one item.  When old
+    // heads are replicated (TP_old > H) several old ranks hold the same head and
+    // one of them is the source: the destination itself if it holds a replica
+    // (a local copy), else replica (new replica index mod old replicas), which
+    // spreads the sends over the replicas.
     const Ownership& O = p->own_old;
     const Ownership& N = p->own_new;
     const int64_t row = static_cast<int64_t>(s.head_dim) * s.elem_bytes;
@@ -166,13 +172,24 @@ remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo, c
     for (int32_t l = 0; l < s.num_layers; ++l) {
         const int32_t old_stage = O.pp_owner(l), new_stage = N.pp_owner(l);
         for (int32_t ntp = 0; ntp < N.tp; ++ntp) {
-            const int32_t t0 = ntp * N.heads_per_rank(), t1 = t0 + N.heads_per_rank();
-            for (int32_t otp = 0; otp < O.tp; ++otp) {
-                const int32_t s0 = otp * O.heads_per_rank(), s1 = s0 + O.heads_per_rank();
-                const int32_t h0 = std::max(t0, s0), h1 = std::min(t1, s1);
-                if (h0 >= h1) continue;
-                Item it{O.rank(old_stage, otp), N.rank(new_stage, ntp), l, h0, h1 - h0, -1};
-                p->items.push_back(it);
+            const int32_t t0 = N.first_head_of_tp(ntp), t1 = t0 + N.heads_per_rank();
+            const int32_t dst = N.rank(new_stage, ntp);
+            if (O.replicas() == 1) {
+                for (int32_t otp = 0; otp < O.tp; ++otp) {
+                    const int32_t s0 = O.first_head_of_tp(otp), s1 = s0 + O.heads_per_rank();
+                    const int32_t h0 = std::max(t0, s0), h1 = std::min(t1, s1);
+                    if (h0 >= h1) continue;
+                    p->items.push_back(Item{O.rank(old_stage, otp), dst, l, h0, h1 - h0, -1});
+                }
+                continue;
+            }
+            // replicated old heads: one old head per old rank, choose a replica per target head
+            for (int32_t h = t0; h < t1; ++h) {
+                int32_t otp = -1;
+                for (int32_t k = 0; k < O.replicas(); ++k)
+                    if (O.rank(old_stage, O.tp_of_head(h, k)) == dst) otp = O.tp_of_head(h, k);
+                if (otp < 0) otp = O.tp_of_head(h, N.replica_index(ntp) % O.replicas());
+                p->items.push_back(Item{O.rank(old_stage, otp), dst, l, h, 1, -1});
             }
         }
     }

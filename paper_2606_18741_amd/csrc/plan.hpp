@@ -23,17 +23,26 @@ struct Pair {
     int64_t slice_bytes;
 };
 
+// Ownership of one topology (Section 3.4.1).  Layers: stage p holds
+// [p*L/PP, (p+1)*L/PP).  Heads: with TP <= H, tensor rank t holds
+// [t*H/TP, (t+1)*H/TP); with TP > H (TP a multiple of H, GQA replication) it
+// holds the single head t*H/TP, and each head has TP/H replicas.
 struct Ownership {
     int32_t tp, pp, L, H;
     int32_t layers_per_stage() const { return L / pp; }
-    int32_t heads_per_rank() const { return H / tp; }
+    int32_t heads_per_rank() const { return tp <= H ? H / tp : 1; }
+    int32_t replicas() const { return tp <= H ? 1 : tp / H; }
     int32_t pp_owner(int32_t l) const { return l / layers_per_stage(); }
-    int32_t tp_owner(int32_t h) const { return h / heads_per_rank(); }
     int32_t rank(int32_t stage, int32_t t) const { return stage * tp + t; }
     int32_t stage_of(int32_t r) const { return r / tp; }
     int32_t tp_of(int32_t r) const { return r % tp; }
     int32_t first_layer(int32_t r) const { return stage_of(r) * layers_per_stage(); }
-    int32_t first_head(int32_t r) const { return tp_of(r) * heads_per_rank(); }
+    int32_t first_head_of_tp(int32_t t) const { return static_cast<int32_t>(static_cast<int64_t>(t) * H / tp); }
+    int32_t first_head(int32_t r) const { return first_head_of_tp(tp_of(r)); }
+    // replica index of tensor rank t among the ranks holding its head (0 without replication)
+    int32_t replica_index(int32_t t) const { return tp <= H ? 0 : t % (tp / H); }
+    // tensor rank holding head h as replica k
+    int32_t tp_of_head(int32_t h, int32_t k) const { return tp <= H ? h / (H / tp) : h * (tp / H) + k; }
     int32_t world() const { return tp * pp; }
 };
 

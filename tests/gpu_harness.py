@@ -14,6 +14,7 @@ import torch
 
 import paper_2606_18741_amd as rk
 import synthkv
+from hostpools import local_heads, source_stream_rank
 
 DEV = "cuda:0"
 STAGING_TAG = 99
@@ -51,7 +52,7 @@ class RankPool:
         tp, _ = topo
         self.rank = rank
         self.layers = rank_layers(rank, topo, w.num_layers)
-        H_loc = w.num_kv_heads // tp
+        H_loc = local_heads(w.num_kv_heads, tp)
         dt = synthkv.torch_dtype_for(w.elem_bytes)
         want = set(self.layers if layers is None else layers) & set(self.layers)
         self.store: Dict[int, torch.Tensor] = {}
@@ -61,7 +62,7 @@ class RankPool:
             t = torch.empty((2, tables.num_blocks, tables.block_size, H_loc, w.head_dim), dtype=dt, device=device)
             for kv in range(2):
                 if fill == "source":
-                    synthkv.fill_pool_layer_(t[kv], w.seed, rank, l, kv)
+                    synthkv.fill_pool_layer_(t[kv], w.seed, source_stream_rank(rank, tp, w.num_kv_heads), l, kv)
                 elif fill == "sentinel":
                     synthkv.fill_sentinel_(t[kv], w.seed, tag, rank, l, kv)
                 else:

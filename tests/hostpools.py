@@ -12,7 +12,16 @@ import synthkv
 
 
 def local_heads(H: int, tp: int) -> int:
-    return H // tp
+    return H // tp if tp <= H else 1
+
+
+def source_stream_rank(r: int, tp: int, H: int) -> int:
+    """Stream id of old rank r's contents: replicas of the same head (TP > H)
+    share the lowest replica's stream, so they hold identical bytes."""
+    if tp <= H:
+        return r
+    rep = tp // H
+    return r - (r % tp) % rep
 
 
 def rank_layers(r: int, tp: int, pp: int, L: int):
@@ -21,8 +30,12 @@ def rank_layers(r: int, tp: int, pp: int, L: int):
     return range(p * per, (p + 1) * per)
 
 
-def source_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None):
-    """Old-pool contents for the given old ranks (default: all) and layers."""
+def source_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None, identical_replicas=True):
+    """Old-pool contents for the given old ranks (default: all) and layers.
+
+    identical_replicas=False gives every replica its own bytes (to see which
+    replica a head was taken from).
+    """
     tp, pp = w.old_topo
     H_loc = local_heads(w.num_kv_heads, tp)
     dt = synthkv.torch_dtype_for(w.elem_bytes)
@@ -33,8 +46,9 @@ def source_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None):
             if layers is not None and l not in layers:
                 continue
             t = torch.empty((2, tables.num_blocks, tables.block_size, H_loc, w.head_dim), dtype=dt)
+            key = source_stream_rank(r, tp, w.num_kv_heads) if identical_replicas else r
             for kv in range(2):
-                synthkv.fill_pool_layer_(t[kv], w.seed, r, l, kv)
+                synthkv.fill_pool_layer_(t[kv], w.seed, key, l, kv)
             out[r][l] = t.numpy().view(synthkv.numpy_dtype_for(w.elem_bytes))
     return out
 

@@ -109,31 +109,42 @@ def _check_plan(old, new, L, H, D=8, e=2):
         for q in range(T(*new).world):
             if (r, q) not in want:
                 assert p.query(r, q)[0] == 0
-    # Algorithm 1 emits one item per (layer, new tensor rank, old tensor rank) with overlapping heads
+    # Algorithm 1 emits one item per (layer, new tensor rank, old tensor rank) with overlapping heads;
+    # with replicated old heads, one per (layer, new tensor rank, target head) from the chosen replica
+    def head_range(t, tp):
+        return (t * H // tp, t * H // tp + 1) if tp > H else (t * H // tp, (t + 1) * H // tp)
     items = 0
     for l in range(L):
         for ntp in range(new[0]):
+            a0, a1 = head_range(ntp, new[0])
+            if old[0] > H:
+                items += a1 - a0
+                continue
             for otp in range(old[0]):
-                a0, a1 = ntp * H // new[0], (ntp + 1) * H // new[0]
-                b0, b1 = otp * H // old[0], (otp + 1) * H // old[0]
+                b0, b1 = head_range(otp, old[0])
                 items += max(a0, b0) < min(a1, b1)
     assert p.info.num_items == items == sum(q.layer_end - q.layer_begin for q in p.pairs)
     assert p.info.old_world == old[0] * old[1] and p.info.new_world == new[0] * new[1]
     assert p.info.total_tokens == Tk
 
 
-@pytest.mark.parametrize("L,H", [(4, 8), (6, 12), (8, 8), (80, 8), (32, 32), (40, 40)])
-def test_plan_matches_definition(L, H):
-    for tp_o, pp_o, tp_n, pp_n in itertools.product(_divisors(H)[:5], _divisors(L)[:4], _divisors(H)[:5],
-                                                    _divisors(L)[:4]):
+def _tps(H, k=5):
+    return _divisors(H)[:k] + [2 * H, 4 * H]
+
+
+@pytest.mark.parametrize("L,H,tps", [(4, 8, None), (6, 12, None), (8, 8, None), (80, 8, None), (48, 4, None),
+                                     (4, 1, None), (32, 32, [1, 2, 4, 8, 64]), (40, 40, [1, 2, 4, 8, 80])])
+def test_plan_matches_definition(L, H, tps):
+    tps = tps or _tps(H)
+    for tp_o, pp_o, tp_n, pp_n in itertools.product(tps, _divisors(L)[:3], tps, _divisors(L)[:3]):
         _check_plan((tp_o, pp_o), (tp_n, pp_n), L, H)
 
 
 @settings(max_examples=60, deadline=None)
 @given(st.integers(1, 12), st.integers(1, 12), st.data())
 def test_plan_matches_definition_random(L, H, data):
-    old = (data.draw(st.sampled_from(_divisors(H))), data.draw(st.sampled_from(_divisors(L))))
-    new = (data.draw(st.sampled_from(_divisors(H))), data.draw(st.sampled_from(_divisors(L))))
+    old = (data.draw(st.sampled_from(_tps(H, 99))), data.draw(st.sampled_from(_divisors(L))))
+    new = (data.draw(st.sampled_from(_tps(H, 99))), data.draw(st.sampled_from(_divisors(L))))
     _check_plan(old, new, L, H, D=data.draw(st.integers(1, 9)), e=data.draw(st.sampled_from([1, 2, 4])))
 
 
@@ -169,7 +180,8 @@ def test_plan_errors():
     t = _tables()
     ht = rk.HostTables.of(t)
     shape = (4, 8, 8, 2, 16, 16)
-    _expect("REMP_E_UNSUPPORTED", rk.Plan, (3, 1), (1, 1), shape, ht)        # H % TP
+    _expect("REMP_E_UNSUPPORTED", rk.Plan, (3, 1), (1, 1), shape, ht)        # H % TP and TP % H
+    _expect("REMP_E_UNSUPPORTED", rk.Plan, (12, 1), (1, 1), shape, ht)
     _expect("REMP_E_UNSUPPORTED", rk.Plan, (1, 1), (1, 3), shape, ht)        # L % PP
     _expect("REMP_E_INVALID", rk.Plan, (0, 1), (1, 1), shape, ht)
     _expect("REMP_E_INVALID", rk.Plan, (1, 1), (1, 1), (4, 8, 8, 3, 16, 16), ht)   # elem bytes

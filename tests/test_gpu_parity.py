@@ -75,9 +75,9 @@ def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None, loc
     return plan, src, dst, staging, flags
 
 
-def check_against_oracle(w, inp, windows=None, log_name="", local=False):
+def check_against_oracle(w, inp, windows=None, log_name="", local=False, identical_replicas=True):
     L, H = w.num_layers, w.num_kv_heads
-    old_host = hostpools.source_pools(w, inp.old_tables)
+    old_host = hostpools.source_pools(w, inp.old_tables, identical_replicas=identical_replicas)
     new_host = hostpools.sentinel_pools(w, inp.new_tables)
     log(f"[parity] {log_name or w.name}: T={int(inp.lens.sum())} windows={windows} local={local}")
     plan, src, dst, staging, flags = migrate_all(w, inp.old_tables, inp.new_tables, old_host, new_host, windows,
@@ -112,7 +112,8 @@ def check_against_oracle(w, inp, windows=None, log_name="", local=False):
 # hand-derived examples (expected values written by hand, not by the oracle)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["hand_tp2pp1_to_tp1pp2.json", "hand_tp1pp2_to_tp2pp1_reblock.json"])
+@pytest.mark.parametrize("name", ["hand_tp2pp1_to_tp1pp2.json", "hand_tp1pp2_to_tp2pp1_reblock.json",
+                                  "hand_replicated_tp4_to_tp2.json"])
 def test_golden_hand_example_gpu(name):
     with open(os.path.join(GOLDEN, name)) as f:
         g = json.load(f)
@@ -132,8 +133,8 @@ def test_golden_hand_example_gpu(name):
     for q in range(nt.world):
         for l in rank_layers(q, g["new_topo"], g["num_layers"]):
             new_host.setdefault(q, {})[l] = np.full(
-                (2, g["new_num_blocks"], g["new_block_size"], g["num_kv_heads"] // nt.tp, g["head_dim"]),
-                g["sentinel"], np.uint16)
+                (2, g["new_num_blocks"], g["new_block_size"], len(oracle.heads_of(q, nt, g["num_kv_heads"])),
+                 g["head_dim"]), g["sentinel"], np.uint16)
     log(f"[golden] {name}")
     plan, src, dst, staging, flags = migrate_all(w, old_t, new_t, old_host, new_host)
     assert all(f == 0 for f in flags)
@@ -193,6 +194,13 @@ EDGE = {
     "fragmented_pool": _custom(pool_law=("fragmented", 0.5), num_seqs=12),
     "all_empty": _custom(length_law=("fixed", 0)),
     "many_sequences": _custom(num_seqs=1500, length_law=("uniform", 0, 9), num_layers=2),
+    # GQA with more tensor ranks than KV heads (e.g. 4 KV heads at TP8): heads are replicated
+    "replicated_tp8_to_tp2": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(8, 1), new_topo=(2, 1)),
+    "replicated_tp2pp2_to_tp8": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(2, 2),
+                                        new_topo=(8, 1)),
+    "replicated_tp16_to_tp8pp2": _custom(num_layers=8, num_kv_heads=4, head_dim=64, old_topo=(16, 1),
+                                         new_topo=(8, 2), old_block_size=16, new_block_size=32),
+    "replicated_keep_local": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(8, 1), new_topo=(4, 2)),
 }
 
 
@@ -200,6 +208,19 @@ EDGE = {
 def test_edge_case(name):
     w = EDGE[name]
     check_against_oracle(w, synthkv.make_inputs(w), log_name=name)
+
+
+@pytest.mark.parametrize("name", [n for n in EDGE if n.startswith("replicated")])
+def test_replica_choice_visible(name):
+    """Replicas hold different bytes, so the source replica each new rank used is checked too."""
+    check_against_oracle(EDGE[name], synthkv.make_inputs(EDGE[name]), log_name=name + "_distinct",
+                         identical_replicas=False)
+
+
+@pytest.mark.parametrize("name", ["replicated_tp8_to_tp2", "replicated_keep_local"])
+def test_replica_choice_visible_local(name):
+    check_against_oracle(EDGE[name], synthkv.make_inputs(EDGE[name]), log_name=name + "_distinct_local",
+                         identical_replicas=False, local=True)
 
 
 def test_padded_table_rows():

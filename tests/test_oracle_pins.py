@@ -67,11 +67,16 @@ def _load_golden(name):
     for q in range(new_topo.world):
         for l in oracle.layers_of(q, new_topo, L):
             new_pools.setdefault(q, {})[l] = np.full(
-                (2, g["new_num_blocks"], g["new_block_size"], H // new_topo.tp, D), g["sentinel"], np.uint16)
+                (2, g["new_num_blocks"], g["new_block_size"], len(oracle.heads_of(q, new_topo, H)), D),
+                g["sentinel"], np.uint16)
     return g, old_t, new_t, old_pools, new_pools
 
 
-@pytest.mark.parametrize("name", ["hand_tp2pp1_to_tp1pp2.json", "hand_tp1pp2_to_tp2pp1_reblock.json"])
+GOLDEN_FILES = ["hand_tp2pp1_to_tp1pp2.json", "hand_tp1pp2_to_tp2pp1_reblock.json",
+                "hand_replicated_tp4_to_tp2.json"]
+
+
+@pytest.mark.parametrize("name", GOLDEN_FILES)
 def test_golden_hand_example(name):
     g, old_t, new_t, old_pools, new_pools = _load_golden(name)
     L, H = g["num_layers"], g["num_kv_heads"]
@@ -95,7 +100,7 @@ def test_golden_hand_example(name):
 # identity and round trips
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("topo", [(1, 1), (2, 1), (1, 2), (2, 2), (4, 1)])
+@pytest.mark.parametrize("topo", [(1, 1), (2, 1), (1, 2), (2, 2), (4, 1), (8, 1), (16, 2)])
 def test_identity(topo):
     w, inp = _small(old=topo, new=topo)
     old = hostpools.source_pools(w, inp.old_tables)
@@ -123,7 +128,8 @@ def _live_mask(tables, shape_blocks, bs):
 
 
 @pytest.mark.parametrize("a,b", [((2, 1), (4, 1)), ((4, 1), (1, 1)), ((1, 2), (1, 4)), ((1, 4), (1, 1)),
-                                 ((2, 1), (1, 2)), ((2, 2), (4, 1)), ((1, 4), (4, 1))])
+                                 ((2, 1), (1, 2)), ((2, 2), (4, 1)), ((1, 4), (4, 1)),
+                                 ((2, 1), (8, 1)), ((8, 1), (2, 2)), ((8, 2), (16, 1))])
 @pytest.mark.parametrize("reblock", [False, True])
 def test_round_trip(a, b, reblock):
     w, inp = _small(old=a, new=b, bs_n=4 if reblock else 2, seed=11)
@@ -171,7 +177,8 @@ def _tag_pools(tp, pp, L, H, D, tables, sentinel=0x1234):
     return pools
 
 
-@pytest.mark.parametrize("a,b", [((2, 1), (1, 2)), ((4, 1), (2, 2)), ((1, 4), (2, 1)), ((2, 2), (2, 2))])
+@pytest.mark.parametrize("a,b", [((2, 1), (1, 2)), ((4, 1), (2, 2)), ((1, 4), (2, 1)), ((2, 2), (2, 2)),
+                                 ((2, 1), (8, 1)), ((8, 2), (4, 1))])
 def test_exactly_once_tags(a, b):
     w, inp = _small(L=4, H=4, D=8, old=a, new=b, bs_o=2, bs_n=4, S=4, max_len=9, seed=5)
     L, H, D = w.num_layers, w.num_kv_heads, w.head_dim
@@ -190,8 +197,9 @@ def test_exactly_once_tags(a, b):
                 row = arr[kv, blk, slot, hl]
                 if row[0] == MAGIC:
                     assert row[7] == MAGIC ^ 0xFFFF
-                    tag = (int(row[1]), int(row[2]), int(row[3]) | (int(row[4]) << 16), int(row[5]), int(row[6]))
-                    assert tag not in seen, f"row {tag} written twice"
+                    tag = (int(row[1]), int(row[2]), int(row[3]) | (int(row[4]) << 16), int(row[5]), int(row[6]),
+                           q)
+                    assert tag not in seen, f"row {tag} written twice on rank {q}"
                     seen[tag] = (q, l, blk, slot, hl, kv)
                 else:
                     assert (row == 0x7777).all(), "non-live slot modified"
@@ -201,12 +209,12 @@ def test_exactly_once_tags(a, b):
         toks = bruteforce.slot_list(inp.new_tables.row(s)[: (n + 3) // 4], 4)
         for l in range(L):
             for h in range(H):
-                q = bruteforce.find_rank(own_n, l, h)
-                for t in range(n):
-                    for kv in range(2):
-                        expect += 1
-                        blk, slot = toks[t]
-                        assert seen[(s, l, t, h, kv)] == (q, l, blk, slot, own_n[q][1].index(h), kv)
+                for q in bruteforce.find_ranks(own_n, l, h):           # every holder gets it once
+                    for t in range(n):
+                        for kv in range(2):
+                            expect += 1
+                            blk, slot = toks[t]
+                            assert seen[(s, l, t, h, kv, q)] == (q, l, blk, slot, own_n[q][1].index(h), kv)
     assert len(seen) == expect
 
 
@@ -215,14 +223,20 @@ def test_exactly_once_tags(a, b):
 # ---------------------------------------------------------------------------
 
 CASES = [((2, 1), (1, 2), 2, 2), ((1, 2), (2, 1), 2, 4), ((4, 1), (2, 2), 4, 2), ((2, 2), (1, 4), 2, 2),
-         ((1, 1), (4, 1), 1, 3), ((2, 2), (4, 1), 4, 8)]
+         ((1, 1), (4, 1), 1, 3), ((2, 2), (4, 1), 4, 8),
+         # replicated KV heads (H = 4): TP 8 and 16 hold each head 2 and 4 times
+         ((8, 1), (2, 2), 2, 4), ((2, 2), (8, 1), 2, 2), ((8, 1), (8, 1), 2, 2), ((16, 1), (8, 2), 2, 4),
+         ((8, 2), (16, 1), 4, 2), ((1, 4), (8, 2), 2, 2),
+         # new rank 7 holds head 3 in both topologies: it must keep its own replica, not take old rank 6's
+         ((8, 1), (4, 2), 2, 2)]
 
 
 @pytest.mark.parametrize("a,b,bs_o,bs_n", CASES)
 def test_bruteforce_agrees(a, b, bs_o, bs_n):
     w, inp = _small(old=a, new=b, bs_o=bs_o, bs_n=bs_n, S=3, max_len=11, seed=3)
     L, H = w.num_layers, w.num_kv_heads
-    old = hostpools.source_pools(w, inp.old_tables)
+    # replicas get different bytes so the choice of source replica is visible
+    old = hostpools.source_pools(w, inp.old_tables, identical_replicas=False)
     new_o = hostpools.sentinel_pools(w, inp.new_tables)
     new_b = hostpools.copy_pools(new_o)
     pairs = list(oracle.pair_slices(T(*a), T(*b), L, H))
@@ -274,30 +288,38 @@ def test_library_formulation(a, b):
 @pytest.mark.parametrize("L,H", [(4, 8), (12, 12), (80, 8), (40, 40)])
 def test_staging_bytes_closed_form(L, H):
     D, e, Tk = 128, 2, 1000
-    for tp_o, pp_o, tp_n, pp_n in itertools.product(_divisors(H)[:4], _divisors(L)[:3], _divisors(H)[:4],
-                                                    _divisors(L)[:3]):
+    tps = _divisors(H)[:4] + [2 * H, 4 * H]
+    for tp_o, pp_o, tp_n, pp_n in itertools.product(tps, _divisors(L)[:3], tps, _divisors(L)[:3]):
         a, b = T(tp_o, pp_o), T(tp_n, pp_n)
         sb = oracle.staging_bytes(a, b, L, H, D, e, Tk)
-        # every old rank ships its whole shard; every new rank receives its whole shard
-        for r in range(a.world):
-            assert sum(v for (rr, _), v in sb.items() if rr == r) == 2 * Tk * (L // pp_o) * (H // tp_o) * D * e
+        # every new rank receives its whole shard
+        hn = H // tp_n if tp_n <= H else 1
         for q in range(b.world):
-            assert sum(v for (_, qq), v in sb.items() if qq == q) == 2 * Tk * (L // pp_n) * (H // tp_n) * D * e
-        assert sum(sb.values()) == 2 * Tk * L * H * D * e
+            assert sum(v for (_, qq), v in sb.items() if qq == q) == 2 * Tk * (L // pp_n) * hn * D * e
+        assert sum(sb.values()) == 2 * Tk * L * max(H, tp_n) * D * e
+        # without old replication every old rank ships its whole shard, once per new replica of a head
+        if tp_o <= H:
+            rep_n = max(1, tp_n // H)
+            for r in range(a.world):
+                assert sum(v for (rr, _), v in sb.items() if rr == r) == \
+                    2 * Tk * (L // pp_o) * (H // tp_o) * D * e * rep_n
 
 
 def test_pair_slices_match_explicit_grouping():
-    for L, H in [(4, 4), (6, 12), (8, 8)]:
-        for tp_o, pp_o, tp_n, pp_n in itertools.product(_divisors(H), _divisors(L), _divisors(H), _divisors(L)):
+    for L, H in [(4, 4), (6, 12), (8, 8), (4, 2)]:
+        tps = _divisors(H) + [2 * H, 4 * H]
+        for tp_o, pp_o, tp_n, pp_n in itertools.product(tps, _divisors(L), tps, _divisors(L)):
             own_o = bruteforce.explicit_ownership(tp_o, pp_o, L, H)
             own_n = bruteforce.explicit_ownership(tp_n, pp_n, L, H)
             want = {}
-            for r, (lo, ho) in enumerate(own_o):
-                for q, (ln, hn) in enumerate(own_n):
-                    ls = sorted(set(lo) & set(ln))
-                    hs = sorted(set(ho) & set(hn))
-                    if ls and hs:
-                        want[(r, q)] = (ls, hs)
+            for q, (ln, hn) in enumerate(own_n):
+                for l in ln:
+                    for h in hn:
+                        r = bruteforce.supplier(own_o, own_n, l, h, q)
+                        ls, hs = want.setdefault((r, q), (set(), set()))
+                        ls.add(l)
+                        hs.add(h)
+            want = {k: (sorted(v[0]), sorted(v[1])) for k, v in want.items()}
             assert oracle.pair_slices(T(tp_o, pp_o), T(tp_n, pp_n), L, H) == want
 
 
@@ -345,10 +367,12 @@ def test_point_queries_agree_with_reshard():
 
 def _pins_pass():
     try:
-        test_golden_hand_example("hand_tp2pp1_to_tp1pp2.json")
-        test_golden_hand_example("hand_tp1pp2_to_tp2pp1_reblock.json")
+        for g in GOLDEN_FILES:
+            test_golden_hand_example(g)
         test_bruteforce_agrees((4, 1), (2, 2), 4, 2)
         test_bruteforce_agrees((1, 2), (2, 1), 2, 4)
+        test_bruteforce_agrees((16, 1), (8, 2), 2, 4)
+        test_bruteforce_agrees((8, 1), (4, 2), 2, 2)
         test_round_trip((2, 1), (1, 2), True)
     except Exception:          # a failed assertion or a crash both count as caught
         return False
@@ -379,15 +403,26 @@ def _wrong_pp_owner(l, topo, L):
     return l % topo.pp                        # round-robin layers instead of contiguous ranges
 
 
-def _wrong_tp_owner(h, topo, H):
-    return h % topo.tp                        # round-robin heads instead of contiguous ranges
+def _wrong_tp_owners(h, topo, H):
+    return [h % topo.tp] if topo.tp <= H else _orig_tp_owners(h, topo, H)   # round-robin heads
 
 
-def _swapped_kv_materialise(*args, **kw):
-    return _orig_materialise(*args, **kw)[::-1]    # K and V exchanged
+def _swapped_kv_gather(*args, **kw):
+    return _orig_gather(*args, **kw)[::-1]    # K and V exchanged
 
 
-_orig_materialise = ors.materialise
+def _wrong_source_first(l, h, q, old, new, L, H):
+    cands = ors.holders(l, h, old, L, H)
+    return q if q in cands else cands[0]              # always the first replica
+
+
+def _wrong_source_nolocal(l, h, q, old, new, L, H):
+    cands = ors.holders(l, h, old, L, H)
+    return cands[ors.holders(l, h, new, L, H).index(q) % len(cands)]    # no local preference
+
+
+_orig_gather = ors.gather_rows
+_orig_tp_owners = ors.tp_owners
 _orig_token_slots = ors.token_slots
 _orig_heads_of = ors.heads_of
 _orig_token_offsets = ors.token_offsets
@@ -399,8 +434,10 @@ _orig_token_offsets = ors.token_offsets
     ("heads_of", _wrong_heads_of),
     ("token_offsets", _wrong_token_offsets),
     ("pp_owner", _wrong_pp_owner),
-    ("tp_owner", _wrong_tp_owner),
-    ("materialise", _swapped_kv_materialise),
+    ("tp_owners", _wrong_tp_owners),
+    ("gather_rows", _swapped_kv_gather),
+    ("source_of", _wrong_source_first),
+    ("source_of", _wrong_source_nolocal),
 ])
 def test_planted_mistakes_are_caught(monkeypatch, target, mutant):
     assert _pins_pass()

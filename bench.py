@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--cpu-sample-layers", type=int, default=24,
                     help="layers per new pipeline stage in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd", "rocm"],
+                    help="physical layout of both pools (hnd and rocm go through the LDS tile kernel)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (for counter scaling), then exit")
     return ap.parse_args()
@@ -116,6 +118,9 @@ def main() -> int:
     ro, qn = w.role
     L, H, D = w.num_layers, w.num_kv_heads, w.head_dim
     (tpo, ppo), (tpn, ppn) = w.old_topo, w.new_topo
+    layout = {"nhd": rk.LAYOUT_NHD, "hnd": rk.LAYOUT_HND, "rocm": rk.LAYOUT_ROCM_SPLIT}[args.layout]
+    if layout != rk.LAYOUT_NHD:
+        args.no_cpu_baseline = True        # the oracle's sample reads NHD pools
     inp = synthkv.make_inputs(w)
     shape = (L, H, D, w.elem_bytes, w.old_block_size, w.new_block_size)
     plan = rk.Plan(w.old_topo, w.new_topo, shape, rk.HostTables.of(inp.old_tables))
@@ -146,9 +151,10 @@ def main() -> int:
         for kv in range(2):
             synthkv.fill_pool_layer_(t[kv], w.seed, ro, l, kv)
         src_layers[l] = t
-    src_arg = tio.pool_arg([src_layers[l] for l in layers_of(ro, tpo, ppo)], inp.old_tables.num_blocks)
+    # the same bytes serve any layout: the migration is a permutation of them
+    src_arg = tio.pool_arg([src_layers[l] for l in layers_of(ro, tpo, ppo)], inp.old_tables.num_blocks, layout)
     dst_layers = {l: alloc_layer(inp.new_tables, tpn) for l in layers_of(qn, tpn, ppn)}
-    dst_arg = tio.pool_arg([dst_layers[l] for l in layers_of(qn, tpn, ppn)], inp.new_tables.num_blocks)
+    dst_arg = tio.pool_arg([dst_layers[l] for l in layers_of(qn, tpn, ppn)], inp.new_tables.num_blocks, layout)
     dto = tio.DeviceTables(rk.HostTables.of(inp.old_tables), dev)
     dtn = tio.DeviceTables(rk.HostTables.of(inp.new_tables), dev)
     staging = tio.alloc_staging(plan, sorted(set(pairs_out) | set(pairs_in)), dev)
@@ -177,7 +183,7 @@ def main() -> int:
             tmp[l] = t
             if l in keep_layers and pair_info[(r, q)].layer_begin <= l < pair_info[(r, q)].layer_end:
                 foreign_host[(r, l)] = t.cpu().numpy().view(synthkv.numpy_dtype_for(w.elem_bytes))
-        arg = tio.pool_arg([tmp[l] for l in layers_of(r, tpo, ppo)], inp.old_tables.num_blocks)
+        arg = tio.pool_arg([tmp[l] for l in layers_of(r, tpo, ppo)], inp.old_tables.num_blocks, layout)
         extra = tio.alloc_staging(plan, [pp for pp in pair_info if pp[0] == r and pp != (r, q)], dev)
         bufs = dict(extra)
         bufs[(r, q)] = staging[(r, q)]
@@ -229,7 +235,7 @@ def main() -> int:
     # --- the same share with the local fast path (slices old rank ro keeps as new
     # rank qn go pool to pool; the rest through staging), timed the same way
     local = None
-    if ro == qn and (ro, qn) in pair_info:
+    if ro == qn and (ro, qn) in pair_info and layout == rk.LAYOUT_NHD:
         P_local = pair_info[(ro, qn)].staging_bytes
         st_out_r = tio.staging_args({k: v for k, v in staging.items() if k[0] == ro and k[1] != ro}, ro, W_new, True)
         st_in_r = tio.staging_args({k: v for k, v in staging.items() if k[1] == qn and k[0] != qn}, qn, W_old, False)
@@ -322,6 +328,7 @@ def main() -> int:
         "config": {
             "workload": w.name + ": " + w.description,
             "role": f"old rank {ro} packs for all destinations, new rank {qn} unpacks from all sources",
+            "pool_layout": args.layout,
             "total_tokens": plan.info.total_tokens,
             "pack_bytes": P_pack,
             "unpack_bytes": P_unpack,

@@ -111,12 +111,24 @@ typedef struct {
     const int32_t* block_ids;
 } remp_dev_tables;
 
+/* Physical layouts of a layer's K and V storage (H_loc = heads the rank holds). */
+enum {
+    REMP_KV_LAYOUT_NHD = 0,        /* K and V [num_blocks][block_size][H_loc][head_dim] */
+    REMP_KV_LAYOUT_HND = 1,        /* K and V [num_blocks][H_loc][block_size][head_dim] */
+    REMP_KV_LAYOUT_ROCM_SPLIT = 2  /* K [num_blocks][H_loc][head_dim/x][block_size][x], x = 16 / elem_bytes;
+                                      V [num_blocks][H_loc][head_dim][block_size]
+                                      (the ROCm paged-attention cache layout) */
+};
+
 /* A rank's paged KV storage: one K and one V device pointer per local layer
  * (local layer i = global layer first_layer_of_rank + i), each addressing
- * [num_blocks][block_size][H/TP][head_dim] elements.  Pointer arrays are host
- * memory; entries for layers outside the call's layer window may be NULL. */
+ * num_blocks blocks in `layout`.  Pointer arrays are host memory; entries for
+ * layers outside the call's layer window may be NULL.  HND and ROCM_SPLIT need
+ * head_dim * elem_bytes % 16 == 0 and 16-byte aligned storage; ROCM_SPLIT also
+ * block_size * elem_bytes % 16 == 0 (REMP_E_UNSUPPORTED / REMP_E_ALIGN). */
 typedef struct {
     int32_t num_layers;
+    int32_t layout;
     void* const* k;
     void* const* v;
     int64_t num_blocks;
@@ -240,7 +252,8 @@ REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank
  * pool, addressed by new_tables), without staging.  Together with pack and
  * unpack called with REMP_KV_SKIP_LOCAL this yields the same new pool as a
  * staged migration while moving the local share once instead of twice.
- * rank must exist in both topologies.  src and dst storage must not overlap
+ * rank must exist in both topologies; both pools must be NHD
+ * (REMP_E_UNSUPPORTED otherwise).  src and dst storage must not overlap
  * (checked per layer, REMP_E_INVALID).  new_tables are validated as in
  * remp_kv_unpack.  old_tables / new_dev_tables: device copies of the tables.
  * The workspace is the one remp_kv_workspace_bytes sizes; nothing is enqueued

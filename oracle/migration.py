@@ -300,3 +300,47 @@ def staging_location(r: int, q: int, l: int, kv: int, h: int, s: int, t: int, ol
     slice_bytes = 2 * T * len(hs) * D * elem_bytes
     row = (kv * T + int(tok_off[s]) + t) * len(hs) + hs.index(h)
     return ls.index(l) * slice_bytes + row * D * elem_bytes
+
+
+# ---------------------------------------------------------------------------
+# physical pool layouts (encodings of the [2, nb, bs, H_loc, D] logical arrays)
+# ---------------------------------------------------------------------------
+
+NHD, HND, ROCM_SPLIT = 0, 1, 2
+
+
+def encode_pool(arr: np.ndarray, layout: int) -> np.ndarray:
+    """Physical layout of one rank-layer storage [2 (K, V), nb, bs, H_loc, D].
+
+    NHD: K and V [nb][bs][H][D] (unchanged).  HND: K and V [nb][H][bs][D].
+    ROCM_SPLIT (the ROCm paged-attention cache): K [nb][H][D/x][bs][x] with x
+    the number of elements in 16 bytes, V [nb][H][D][bs].  Returns a tuple-like
+    pair (K array, V array) stacked when shapes agree, else a list.
+    """
+    k, v = arr[0], arr[1]
+    if layout == NHD:
+        return [k.copy(), v.copy()]
+    if layout == HND:
+        return [np.ascontiguousarray(k.transpose(0, 2, 1, 3)), np.ascontiguousarray(v.transpose(0, 2, 1, 3))]
+    if layout == ROCM_SPLIT:
+        nb, bs, h, d = k.shape
+        x = 16 // k.dtype.itemsize
+        ks = k.reshape(nb, bs, h, d // x, x).transpose(0, 2, 3, 1, 4)
+        vs = v.transpose(0, 2, 3, 1)
+        return [np.ascontiguousarray(ks), np.ascontiguousarray(vs)]
+    raise ValueError(f"unknown layout {layout}")
+
+
+def decode_pool(kv, layout: int) -> np.ndarray:
+    """Inverse of encode_pool: [2, nb, bs, H_loc, D]."""
+    k, v = kv
+    if layout == NHD:
+        return np.stack([k, v])
+    if layout == HND:
+        return np.stack([k.transpose(0, 2, 1, 3), v.transpose(0, 2, 1, 3)])
+    if layout == ROCM_SPLIT:
+        nb, h, dx, bs, x = k.shape
+        kk = k.transpose(0, 3, 1, 2, 4).reshape(nb, bs, h, dx * x)
+        vv = v.transpose(0, 3, 1, 2)
+        return np.stack([kk, vv])
+    raise ValueError(f"unknown layout {layout}")

@@ -56,8 +56,11 @@ class DevTables(Structure):
 
 
 class Pool(Structure):
-    _fields_ = [("num_layers", c_int32), ("k", POINTER(c_void_p)), ("v", POINTER(c_void_p)),
+    _fields_ = [("num_layers", c_int32), ("layout", c_int32), ("k", POINTER(c_void_p)), ("v", POINTER(c_void_p)),
                 ("num_blocks", c_int64)]
+
+
+LAYOUT_NHD, LAYOUT_HND, LAYOUT_ROCM_SPLIT = 0, 1, 2
 
 
 class Buffer(Structure):
@@ -197,13 +200,13 @@ def dev_tables(seq_lens, row_offsets, block_ids) -> DevTables:
 class PoolArg:
     """A rank's paged storage: K and V device addresses per local layer (None allowed)."""
 
-    def __init__(self, k: Sequence, v: Sequence, num_blocks: int):
+    def __init__(self, k: Sequence, v: Sequence, num_blocks: int, layout: int = LAYOUT_NHD):
         assert len(k) == len(v)
         n = len(k)
         self._k = (c_void_p * max(n, 1))(*[_ptr(x) for x in k])
         self._v = (c_void_p * max(n, 1))(*[_ptr(x) for x in v])
-        self.c = Pool(n, ctypes.cast(self._k, POINTER(c_void_p)), ctypes.cast(self._v, POINTER(c_void_p)),
-                      int(num_blocks))
+        self.c = Pool(n, int(layout), ctypes.cast(self._k, POINTER(c_void_p)),
+                      ctypes.cast(self._v, POINTER(c_void_p)), int(num_blocks))
 
 
 def buffers(entries: Sequence[Optional[Tuple[object, int]]]):

@@ -399,6 +399,210 @@ __global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// head-tile copy through LDS, for pools whose token rows are not contiguous
+// ---------------------------------------------------------------------------
+//
+// Layouts other than NHD keep each (block, head) as one contiguous tile of
+// block_size * head_dim elements: HND stores it token-major ([slot][dim]);
+// the ROCm paged-attention cache stores K as [dim / x][slot][x] (x = the
+// elements in 16 bytes) and V as [dim][slot].  The staging side is always
+// token-major.  A workgroup stages a few tiles in LDS in token-major order
+// (rows padded by 16 bytes against bank conflicts), so both HBM sides are
+// read and written as 16-byte vectors in their own contiguous order.
+
+enum : int32_t { kLayoutNHD = 0, kLayoutHND = 1, kLayoutRocmSplit = 2 };
+constexpr int kTileThreads = 256;
+constexpr int kTileLdsBytes = 32 * 1024;   // dynamic LDS per workgroup, at most
+constexpr int64_t kTileWgBytes = 16 * 1024; // payload bytes a tile workgroup aims to move
+
+struct TileArgs {
+    const BlockDesc* desc;
+    int64_t block_stride;      // paged bytes per block
+    int64_t total_tokens;
+    int32_t n_desc;
+    int32_t tiles_per_wg;
+    int32_t block_size;
+    int32_t head_bytes;        // head_dim * elem_bytes
+    int32_t elem_bytes;
+    int32_t layout;
+    int32_t lds_row;           // head_bytes + 16
+    uint32_t vpt_magic, vpt_shift;   // division by vectors per tile
+    uint32_t vph_magic, vph_shift;   // division by vectors per head row
+    uint32_t bs_magic, bs_shift;     // division by block_size
+    CopyItem items[kMaxItems];       // paged_k/v: the slice's first head tile of the layer's block 0
+};
+static_assert(sizeof(TileArgs) < 4096, "tile kernel arguments must stay below 4 KiB");
+
+
+// Move the elements of one 16-byte vector (consecutive slots of one dim) to or
+// from LDS rows `lrow` bytes apart.
+template <typename E>
+__device__ __forceinline__ void scatter_t(const unsigned int __attribute__((ext_vector_type(4))) & val,
+                                          unsigned char* p, uint32_t lrow) {
+    const E* e = reinterpret_cast<const E*>(&val);
+#pragma unroll
+    for (int k = 0; k < 16 / static_cast<int>(sizeof(E)); ++k) *reinterpret_cast<E*>(p + k * lrow) = e[k];
+}
+
+template <typename E>
+__device__ __forceinline__ unsigned int __attribute__((ext_vector_type(4))) gather_t(const unsigned char* p,
+                                                                                      uint32_t lrow) {
+    unsigned int __attribute__((ext_vector_type(4))) val;
+    E* e = reinterpret_cast<E*>(&val);
+#pragma unroll
+    for (int k = 0; k < 16 / static_cast<int>(sizeof(E)); ++k) e[k] = *reinterpret_cast<const E*>(p + k * lrow);
+    return val;
+}
+
+__device__ __forceinline__ void scatter_dim(const unsigned int __attribute__((ext_vector_type(4))) & val,
+                                            unsigned char* p, uint32_t lrow, int32_t eb) {
+    if (eb == 2) scatter_t<unsigned short>(val, p, lrow);
+    else if (eb == 4) scatter_t<unsigned int>(val, p, lrow);
+    else scatter_t<unsigned char>(val, p, lrow);
+}
+
+__device__ __forceinline__ unsigned int __attribute__((ext_vector_type(4))) gather_dim(const unsigned char* p,
+                                                                                        uint32_t lrow, int32_t eb) {
+    if (eb == 2) return gather_t<unsigned short>(p, lrow);
+    if (eb == 4) return gather_t<unsigned int>(p, lrow);
+    return gather_t<unsigned char>(p, lrow);
+}
+
+// Store the first `nbytes` bytes of a vector (whole elements of eb bytes).
+__device__ __forceinline__ void store_prefix(const unsigned int __attribute__((ext_vector_type(4))) & val,
+                                             void* dst, int32_t nbytes, int32_t eb) {
+    const unsigned char* b = reinterpret_cast<const unsigned char*>(&val);
+    unsigned char* o = reinterpret_cast<unsigned char*>(dst);
+    if (eb == 4) {
+        for (int q = 0; q < nbytes; q += 4)
+            *reinterpret_cast<unsigned int*>(o + q) = *reinterpret_cast<const unsigned int*>(b + q);
+    } else if (eb == 2) {
+        for (int q = 0; q < nbytes; q += 2)
+            *reinterpret_cast<unsigned short*>(o + q) = *reinterpret_cast<const unsigned short*>(b + q);
+    } else {
+        for (int q = 0; q < nbytes; ++q) o[q] = b[q];
+    }
+}
+
+template <bool PACK>
+__global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) {
+    typedef unsigned int V4 __attribute__((ext_vector_type(4)));
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+    __shared__ uint64_t s_paged[kMaxUnitsPerWg];
+    __shared__ uint64_t s_stage[kMaxUnitsPerWg];
+    __shared__ int32_t s_n[kMaxUnitsPerWg];
+    __shared__ int32_t s_kv[kMaxUnitsPerWg];
+
+    const CopyItem& it = args.items[blockIdx.y];
+    const int32_t hc = static_cast<int32_t>(it.row_bytes) / args.head_bytes;   // heads in the slice
+    const int64_t ntiles = static_cast<int64_t>(args.n_desc) * 2 * hc;
+    const int64_t g0 = static_cast<int64_t>(blockIdx.x) * args.tiles_per_wg;
+    if (g0 >= ntiles) return;
+    const int32_t nt = static_cast<int32_t>(min(static_cast<int64_t>(args.tiles_per_wg), ntiles - g0));
+    const int tid = threadIdx.x;
+    const int32_t bs = args.block_size, hb = args.head_bytes;
+    const uint64_t tile_bytes = static_cast<uint64_t>(bs) * hb;
+    const uint64_t kv_stride = static_cast<uint64_t>(args.total_tokens) * it.row_bytes;
+
+    for (int i = tid; i < nt; i += kTileThreads) {
+        const int64_t g = g0 + i;
+        const int64_t d = g / (2 * hc);
+        const int32_t r = static_cast<int32_t>(g - d * 2 * hc);
+        const int32_t kv = r / hc, j = r - (r / hc) * hc;
+        const BlockDesc bd = args.desc[d];
+        s_paged[i] = (kv ? it.paged_v : it.paged_k) + static_cast<uint64_t>(bd.block) * args.block_stride +
+                     static_cast<uint64_t>(j) * tile_bytes;
+        s_stage[i] = it.stage + kv * kv_stride + static_cast<uint64_t>(bd.tok) * it.row_bytes +
+                     static_cast<uint64_t>(j) * hb;
+        s_n[i] = bd.n;
+        s_kv[i] = kv;
+    }
+    __syncthreads();
+
+    const uint32_t vpt = static_cast<uint32_t>(tile_bytes / 16);     // 16-byte vectors per tile
+    const uint32_t vph = static_cast<uint32_t>(hb / 16);             // 16-byte vectors per head row
+    const uint32_t total = static_cast<uint32_t>(nt) * vpt;
+    const uint32_t lrow = static_cast<uint32_t>(args.lds_row);
+    const int32_t m = 16 / args.elem_bytes;                          // elements per vector
+    const uint32_t tile_lds = static_cast<uint32_t>(bs) * lrow;
+
+    // phase 1: fill LDS (token-major)
+    for (uint32_t x = tid; x < total; x += kTileThreads) {
+        const uint32_t i = fast_div(x, args.vpt_magic, args.vpt_shift);
+        const uint32_t v = x - i * vpt;
+        unsigned char* tl = lds + i * tile_lds;
+        if (PACK) {
+            const V4* src = reinterpret_cast<const V4*>(s_paged[i] + uint64_t(v) * 16);
+            if (args.layout == kLayoutHND) {
+                const uint32_t srow = fast_div(v, args.vph_magic, args.vph_shift);
+                if (static_cast<int32_t>(srow) < s_n[i])
+                    *reinterpret_cast<V4*>(tl + srow * lrow + (v - srow * vph) * 16) = __builtin_nontemporal_load(src);
+            } else if (s_kv[i] == 0) {                                    // [dim / x][slot][x]
+                const uint32_t c = fast_div(v, args.bs_magic, args.bs_shift);
+                const uint32_t srow = v - c * bs;
+                if (static_cast<int32_t>(srow) < s_n[i])
+                    *reinterpret_cast<V4*>(tl + srow * lrow + c * 16) = __builtin_nontemporal_load(src);
+            } else {                                                      // [dim][slot]
+                const uint32_t e0 = v * m;
+                const uint32_t dim = fast_div(e0, args.bs_magic, args.bs_shift);
+                const uint32_t s0 = e0 - dim * bs;
+                if (static_cast<int32_t>(s0) < s_n[i])
+                    scatter_dim(__builtin_nontemporal_load(src), tl + s0 * lrow + dim * args.elem_bytes, lrow,
+                                args.elem_bytes);
+            }
+        } else {
+            const uint32_t srow = fast_div(v, args.vph_magic, args.vph_shift);
+            const uint32_t cb = v - srow * vph;
+            if (static_cast<int32_t>(srow) < s_n[i]) {
+                const V4 val = __builtin_nontemporal_load(
+                    reinterpret_cast<const V4*>(s_stage[i] + uint64_t(srow) * it.row_bytes + cb * 16));
+                *reinterpret_cast<V4*>(tl + srow * lrow + cb * 16) = val;
+            }
+        }
+    }
+    __syncthreads();
+
+    // phase 2: drain LDS
+    for (uint32_t x = tid; x < total; x += kTileThreads) {
+        const uint32_t i = fast_div(x, args.vpt_magic, args.vpt_shift);
+        const uint32_t v = x - i * vpt;
+        const unsigned char* tl = lds + i * tile_lds;
+        if (PACK) {
+            const uint32_t srow = fast_div(v, args.vph_magic, args.vph_shift);
+            const uint32_t cb = v - srow * vph;
+            if (static_cast<int32_t>(srow) < s_n[i])
+                __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + srow * lrow + cb * 16),
+                                            reinterpret_cast<V4*>(s_stage[i] + uint64_t(srow) * it.row_bytes + cb * 16));
+        } else {
+            V4* dst = reinterpret_cast<V4*>(s_paged[i] + uint64_t(v) * 16);
+            if (args.layout == kLayoutHND) {
+                const uint32_t srow = fast_div(v, args.vph_magic, args.vph_shift);
+                if (static_cast<int32_t>(srow) < s_n[i])
+                    __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + srow * lrow + (v - srow * vph) * 16), dst);
+            } else if (s_kv[i] == 0) {
+                const uint32_t c = fast_div(v, args.bs_magic, args.bs_shift);
+                const uint32_t srow = v - c * bs;
+                if (static_cast<int32_t>(srow) < s_n[i])
+                    __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + srow * lrow + c * 16), dst);
+            } else {
+                const uint32_t e0 = v * m;
+                const uint32_t dim = fast_div(e0, args.bs_magic, args.bs_shift);
+                const uint32_t s0 = e0 - dim * bs;
+                const int32_t live = min(m, s_n[i] - static_cast<int32_t>(s0));
+                if (live <= 0) continue;
+                const V4 val = gather_dim(tl + s0 * lrow + dim * args.elem_bytes, lrow, args.elem_bytes);
+                if (live == m) {
+                    __builtin_nontemporal_store(val, dst);
+                } else {                                                  // only the live slots
+                    store_prefix(val, dst, live * args.elem_bytes, args.elem_bytes);
+                }
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // host launch code
 // ---------------------------------------------------------------------------
@@ -524,6 +728,69 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     return REMP_OK;
 }
 
+
+template <bool PACK>
+static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostSlice>& slices, int64_t n_desc,
+                                int32_t bs, int64_t block_stride, int32_t layout, const char* ws, int64_t desc_off,
+                                hipStream_t stream) {
+    if (slices.empty() || n_desc == 0) return REMP_OK;
+    if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
+    const int32_t eb = p.shape.elem_bytes;
+    const int64_t hb = static_cast<int64_t>(p.shape.head_dim) * eb;
+    uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(hb);
+    int32_t max_hc = 1;
+    for (const HostSlice& s : slices) {
+        bits |= s.paged_k | s.paged_v | s.stage;
+        max_hc = std::max<int32_t>(max_hc, static_cast<int32_t>(s.row_bytes / hb));
+    }
+    if (bits & 15) return fail(REMP_E_ALIGN, "head-tile layouts need 16-byte aligned storage, staging and head rows");
+    const int64_t tile_bytes = bs * hb, lrow = hb + 16, tile_lds = bs * lrow;
+    if (tile_lds > kTileLdsBytes) return fail(REMP_E_UNSUPPORTED, "a (block, head) tile does not fit in LDS");
+    const int32_t tpw = static_cast<int32_t>(std::max<int64_t>(
+        1, std::min<int64_t>({kTileWgBytes / tile_bytes, kTileLdsBytes / tile_lds, int64_t(kMaxUnitsPerWg)})));
+    const int64_t gx = (n_desc * 2 * max_hc + tpw - 1) / tpw;
+    if (gx > 0x7FFFFFFF) return fail(REMP_E_UNSUPPORTED, "too many tiles for one launch");
+
+    TileArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.desc = reinterpret_cast<const BlockDesc*>(ws + desc_off);
+    a.block_stride = block_stride;
+    a.total_tokens = p.total_tokens;
+    a.n_desc = static_cast<int32_t>(n_desc);
+    a.tiles_per_wg = tpw;
+    a.block_size = bs;
+    a.head_bytes = static_cast<int32_t>(hb);
+    a.elem_bytes = eb;
+    a.layout = layout;
+    a.lds_row = static_cast<int32_t>(lrow);
+    const FastDiv fvpt = make_fastdiv(static_cast<uint32_t>(tile_bytes / 16));
+    const FastDiv fvph = make_fastdiv(static_cast<uint32_t>(hb / 16));
+    const FastDiv fbs = make_fastdiv(static_cast<uint32_t>(bs));
+    a.vpt_magic = fvpt.magic;
+    a.vpt_shift = fvpt.shift;
+    a.vph_magic = fvph.magic;
+    a.vph_shift = fvph.shift;
+    a.bs_magic = fbs.magic;
+    a.bs_shift = fbs.shift;
+    if (g_trace_start) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
+    }
+    for (size_t first = 0; first < slices.size(); first += kMaxItems) {
+        const size_t cnt = std::min<size_t>(kMaxItems, slices.size() - first);
+        for (size_t i = 0; i < cnt; ++i) {
+            const HostSlice& s = slices[first + i];
+            a.items[i] = CopyItem{s.paged_k, s.paged_v, s.stage, s.row_bytes, 0, 0, 0, 0};
+        }
+        const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
+        hipLaunchKernelGGL((copy_tiles<PACK>), grid, dim3(kTileThreads), static_cast<size_t>(tpw * tile_lds), stream, a);
+        if (remp_status st = hip_check(hipGetLastError(), PACK ? "pack tile launch" : "unpack tile launch")) return st;
+    }
+    if (g_trace_stop) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_stop, stream), "trace stop event")) return st;
+    }
+    return REMP_OK;
+}
+
 static bool aligned(const void* p, int64_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 static remp_status check_window(const remp_kv_plan_t* plan, int32_t l0, int32_t l1) {
@@ -533,8 +800,16 @@ static remp_status check_window(const remp_kv_plan_t* plan, int32_t l0, int32_t 
     return REMP_OK;
 }
 
-static remp_status check_pool(const remp_kv_pool* pool, int32_t layers_per_rank, const char* what) {
+static remp_status check_pool(const remp_kv_plan_t* plan, const remp_kv_pool* pool, int32_t layers_per_rank,
+                              int32_t block_size, const char* what) {
     if (!pool) return fail(REMP_E_INVALID, std::string(what) + " pool is NULL");
+    if (pool->layout != kLayoutNHD && pool->layout != kLayoutHND && pool->layout != kLayoutRocmSplit)
+        return fail(REMP_E_INVALID, std::string(what) + " pool has an unknown layout");
+    const int64_t hb = static_cast<int64_t>(plan->shape.head_dim) * plan->shape.elem_bytes;
+    if (pool->layout != kLayoutNHD && hb % 16 != 0)
+        return fail(REMP_E_UNSUPPORTED, std::string(what) + " pool layout needs head_dim * elem_bytes % 16 == 0");
+    if (pool->layout == kLayoutRocmSplit && (static_cast<int64_t>(block_size) * plan->shape.elem_bytes) % 16 != 0)
+        return fail(REMP_E_UNSUPPORTED, std::string(what) + " pool layout needs block_size * elem_bytes % 16 == 0");
     if (pool->num_layers != layers_per_rank)
         return fail(REMP_E_INVALID, std::string(what) + " pool has " + std::to_string(pool->num_layers) +
                                         " layers, the rank holds " + std::to_string(layers_per_rank));
@@ -637,7 +912,10 @@ static remp_status collect_slices(const remp_kv_plan_t& p, bool pack, int32_t ra
         if (!k || !v)
             return fail(REMP_E_INVALID, "pool storage of layer " + std::to_string(it.layer) + " is NULL");
         if (!aligned(k, eb) || !aligned(v, eb)) return fail(REMP_E_ALIGN, "pool storage not element aligned");
-        const int64_t hoff = static_cast<int64_t>(it.head_begin - mine.first_head(rank)) * hrow;
+        const int64_t hstep = pool.layout == kLayoutNHD
+                                  ? hrow
+                                  : hrow * (pack ? p.shape.old_block_size : p.shape.new_block_size);
+        const int64_t hoff = static_cast<int64_t>(it.head_begin - mine.first_head(rank)) * hstep;
         HostSlice s;
         s.paged_k = reinterpret_cast<uint64_t>(k) + hoff;
         s.paged_v = reinterpret_cast<uint64_t>(v) + hoff;
@@ -769,7 +1047,9 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
         return fail(REMP_E_RANGE, "old_rank " + std::to_string(old_rank) + " outside [0, " +
                                       std::to_string(plan->own_old.world()) + ")");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(src, plan->own_old.layers_per_stage(), "source")) return st;
+    if (remp_status st = check_pool(plan, src, plan->own_old.layers_per_stage(), plan->shape.old_block_size,
+                                    "source"))
+        return st;
     if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
     if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     if (src->num_blocks < plan->old_num_blocks)
@@ -788,6 +1068,9 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
     if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz, plan->old_num_blocks,
                                        plan->old_live_blocks, ws, L.scan_old, L.desc_old, true, stream))
         return st;
+    if (src->layout != kLayoutNHD)
+        return launch_tiles<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size,
+                                  row_stride * sh.old_block_size, src->layout, ws, L.desc_old, stream);
     return launch_copy<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size, row_stride * sh.old_block_size,
                              static_cast<int32_t>(row_stride), ws, L.desc_old, stream);
 }
@@ -803,7 +1086,9 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
         return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
                                       std::to_string(plan->own_new.world()) + ")");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(dst, plan->own_new.layers_per_stage(), "destination")) return st;
+    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_per_stage(), plan->shape.new_block_size,
+                                    "destination"))
+        return st;
     if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
     if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     int64_t nnz = 0;
@@ -822,6 +1107,9 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
     if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
                                        plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream))
         return st;
+    if (dst->layout != kLayoutNHD)
+        return launch_tiles<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size,
+                                   row_stride * sh.new_block_size, dst->layout, ws, L.desc_new, stream);
     return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
                               static_cast<int32_t>(row_stride), ws, L.desc_new, stream);
 }
@@ -835,8 +1123,14 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
     if (rank < 0 || rank >= plan->own_old.world() || rank >= plan->own_new.world())
         return fail(REMP_E_RANGE, "rank " + std::to_string(rank) + " is not a rank of both topologies");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(src, plan->own_old.layers_per_stage(), "source")) return st;
-    if (remp_status st = check_pool(dst, plan->own_new.layers_per_stage(), "destination")) return st;
+    if (remp_status st = check_pool(plan, src, plan->own_old.layers_per_stage(), plan->shape.old_block_size,
+                                    "source"))
+        return st;
+    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_per_stage(), plan->shape.new_block_size,
+                                    "destination"))
+        return st;
+    if (src->layout != kLayoutNHD || dst->layout != kLayoutNHD)
+        return fail(REMP_E_UNSUPPORTED, "the local copy handles NHD pools only");
     if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     if (src->num_blocks < plan->old_num_blocks)
         return fail(REMP_E_SIZE, "source pool has fewer blocks than the old tables address");

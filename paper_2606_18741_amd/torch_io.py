@@ -23,11 +23,12 @@ class DeviceTables:
         self.dev = rk.dev_tables(self.lens, self.offs, self.ids)
 
 
-def pool_arg(layers: Sequence[Optional[torch.Tensor]], num_blocks: int) -> rk.PoolArg:
-    """PoolArg from one [2, num_blocks, block_size, H_loc, head_dim] tensor (K, V) per local layer."""
+def pool_arg(layers: Sequence[Optional[torch.Tensor]], num_blocks: int, layout: int = rk.LAYOUT_NHD) -> rk.PoolArg:
+    """PoolArg from one tensor per local layer holding K at [0] and V at [1] in `layout`
+    (e.g. [2, num_blocks, block_size, H_loc, head_dim] for NHD)."""
     ks = [None if t is None else t[0] for t in layers]
     vs = [None if t is None else t[1] for t in layers]
-    return rk.PoolArg(ks, vs, num_blocks)
+    return rk.PoolArg(ks, vs, num_blocks, layout)
 
 
 def alloc_staging(plan: rk.Plan, pairs, device="cuda",

@@ -388,3 +388,26 @@ def test_one_hip_runtime_in_process():
     rk.load()
     runtimes = rk._lib._mapped_hip_runtimes()
     assert len(runtimes) == 1, runtimes
+
+
+@cpu_only
+def test_layout_validation_errors():
+    s = _setup(D=8)          # head_dim 8 * 2 bytes = 16: tile layouts allowed
+    p, L = s["p"], s["L"]
+
+    def pack(src):
+        rk.remp_kv_pack(p.handle, 0, 0, L, src, s["dev"], rk.buffers(s["out0"]), s["ws"], s["ws_bytes"], 0, 0)
+
+    k, v = list(s["src"]._k), list(s["src"]._v)
+    _expect("REMP_E_INVALID", pack, rk.PoolArg(k, v, 64, layout=7))
+    s4 = _setup(D=4)         # 8-byte head rows cannot use the tile layouts
+    k4, v4 = list(s4["src"]._k), list(s4["src"]._v)
+    with pytest.raises(rk.RempError) as ei:
+        rk.remp_kv_pack(s4["p"].handle, 0, 0, s4["L"], rk.PoolArg(k4, v4, 64, layout=rk.LAYOUT_HND), s4["dev"],
+                        rk.buffers(s4["out0"]), s4["ws"], s4["ws_bytes"], 0, 0)
+    assert ei.value.status_name == "REMP_E_UNSUPPORTED"
+    # the local copy is NHD only
+    with pytest.raises(rk.RempError) as ei:
+        rk.remp_kv_copy_local(p.handle, 0, 0, L, rk.PoolArg(k, v, 64, layout=rk.LAYOUT_HND), s["dev"], s["dst"],
+                              rk.HostTables.of(s["new_t"]), s["dev"], s["ws"], s["ws_bytes"], 0)
+    assert ei.value.status_name == "REMP_E_UNSUPPORTED"

@@ -443,3 +443,30 @@ def test_planted_mistakes_are_caught(monkeypatch, target, mutant):
     assert _pins_pass()
     monkeypatch.setattr(ors, target, mutant)
     assert not _pins_pass(), f"pins did not catch a planted mistake in {target}"
+
+
+# ---------------------------------------------------------------------------
+# physical pool layouts
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("layout", [oracle.NHD, oracle.HND, oracle.ROCM_SPLIT])
+@pytest.mark.parametrize("dtype", [np.uint8, np.uint16, np.uint32])
+def test_layout_round_trip(layout, dtype):
+    rng = np.random.default_rng(4)
+    a = rng.integers(0, np.iinfo(dtype).max, size=(2, 5, 8, 3, 32), dtype=dtype)
+    np.testing.assert_array_equal(oracle.decode_pool(oracle.encode_pool(a, layout), layout), a)
+
+
+def test_layout_positions_by_hand():
+    """Element (block 1, slot 3, head 2, dim 10) of a fp16 pool with block 4, 3 heads, head_dim 16:
+    HND puts it at [1][2][3][10]; the ROCm layout puts K at [1][2][10 // 8][3][10 % 8] and V at
+    [1][2][10][3] (x = 16 bytes / 2 = 8 elements)."""
+    a = np.zeros((2, 2, 4, 3, 16), dtype=np.uint16)
+    a[0, 1, 3, 2, 10] = 0xBEEF
+    a[1, 1, 3, 2, 10] = 0xCAFE
+    k, v = oracle.encode_pool(a, oracle.HND)
+    assert k.shape == (2, 3, 4, 16) and k[1, 2, 3, 10] == 0xBEEF and v[1, 2, 3, 10] == 0xCAFE
+    k, v = oracle.encode_pool(a, oracle.ROCM_SPLIT)
+    assert k.shape == (2, 3, 2, 4, 8) and v.shape == (2, 3, 16, 4)
+    assert k[1, 2, 1, 3, 2] == 0xBEEF and v[1, 2, 10, 3] == 0xCAFE
+    assert np.count_nonzero(k) == 1 and np.count_nonzero(v) == 1

@@ -20,7 +20,8 @@
  *
  * Conventions (readings of points the paper leaves open):
  *   - ranks:  rank(pp, tp) = pp * TP + tp;
- *   - layers: stage p of PP holds layers [p*L/PP, (p+1)*L/PP);  L % PP == 0;
+ *   - layers: stage p of PP holds layers [p*L/PP, (p+1)*L/PP) (L % PP == 0),
+ *             or the explicit partition remp_topo.layer_starts;
  *   - heads:  with TP <= H (H % TP == 0) tensor rank t holds KV heads
  *             [t*H/TP, (t+1)*H/TP); with TP > H (TP % H == 0, GQA replication)
  *             it holds the single head t*H/TP, so each head has TP/H replicas;
@@ -62,8 +63,9 @@ extern "C" {
 typedef enum {
     REMP_OK = 0,
     REMP_E_INVALID = -1,     /* malformed argument: null pointer, inconsistent tables, duplicate block id */
-    REMP_E_UNSUPPORTED = -2, /* valid request this version does not handle: L % PP != 0, or TP neither
-                                divides nor is a multiple of the KV head count */
+    REMP_E_UNSUPPORTED = -2, /* valid request this version does not handle: L % PP != 0 without an
+                                explicit partition, or TP neither divides nor is a multiple of the
+                                KV head count */
     REMP_E_RANGE = -3,       /* rank, layer window or block id out of range */
     REMP_E_CAPACITY = -4,    /* the new pool cannot hold the live cache (Section 3.4.5, capacity) */
     REMP_E_ALIGN = -5,       /* a device pointer is not aligned to the element size */
@@ -71,10 +73,16 @@ typedef enum {
     REMP_E_HIP = -7          /* a HIP runtime call or kernel launch failed */
 } remp_status;
 
-/* A parallel topology T = (TP, PP) (Section 3.4.1). */
+/* A parallel topology T = (TP, PP) (Section 3.4.1).  layer_starts (host,
+ * PP + 1 entries, may be NULL) gives an explicit pipeline partition: stage p
+ * holds layers [layer_starts[p], layer_starts[p+1]), starting at 0, ending at
+ * num_layers, every stage holding at least one layer.  NULL means equal
+ * contiguous ranges and then requires num_layers % PP == 0.  The plan copies
+ * the array. */
 typedef struct {
     int32_t tp;
     int32_t pp;
+    const int32_t* layer_starts;
 } remp_topo;
 
 /* Model KV shape.  elem_bytes in {1, 2, 4}.  The block size may differ between

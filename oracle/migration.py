@@ -13,8 +13,9 @@ supplies it and writes it into the new shard, in NumPy.
 
 Readings of points the paper leaves open (each one is listed in the design doc):
 
-* ownership: pp_owner(l, PP) = l // (L / PP) (equal contiguous layer ranges)
-  and rank(pp, tp) = pp * TP + tp, L % PP == 0; heads: with TP <= H
+* ownership: pp_owner(l, PP) = l // (L / PP) (equal contiguous layer ranges,
+  L % PP == 0) unless the topology carries an explicit partition (stage p
+  holds [starts[p], starts[p+1])), and rank(pp, tp) = pp * TP + tp; heads: with TP <= H
   (H % TP == 0) tensor rank t holds [t*H/TP, (t+1)*H/TP); with TP > H
   (TP % H == 0, GQA replication, allowed by the head-coverage invariant of
   Section 3.4.5) it holds the single head t*H/TP, so each head has TP/H
@@ -57,6 +58,7 @@ import numpy as np
 class Topology:
     tp: int
     pp: int
+    starts: Optional[Tuple[int, ...]] = None   # explicit stage boundaries [pp + 1], or equal ranges
 
     @property
     def world(self) -> int:
@@ -66,13 +68,28 @@ class Topology:
 def check_divisible(topo: Topology, L: int, H: int) -> None:
     if topo.tp < 1 or topo.pp < 1:
         raise ValueError("TP and PP must be positive")
-    if L % topo.pp or (H % topo.tp and topo.tp % H):
-        raise ValueError(f"(TP={topo.tp}, PP={topo.pp}) does not fit L={L}, H={H}")
+    if topo.starts is not None:
+        b = list(topo.starts)
+        if len(b) != topo.pp + 1 or b[0] != 0 or b[-1] != L or any(y <= x for x, y in zip(b, b[1:])):
+            raise ValueError(f"bad layer partition {b} for L={L}")
+    elif L % topo.pp:
+        raise ValueError(f"PP={topo.pp} does not divide L={L}")
+    if H % topo.tp and topo.tp % H:
+        raise ValueError(f"TP={topo.tp} does not fit H={H}")
+
+
+def stage_bounds(topo: Topology, L: int) -> List[int]:
+    """First layer of every stage, then L."""
+    if topo.starts is not None:
+        return list(topo.starts)
+    per = L // topo.pp
+    return [p * per for p in range(topo.pp + 1)]
 
 
 def pp_owner(l: int, topo: Topology, L: int) -> int:
     """Pipeline stage that holds layer l."""
-    return l // (L // topo.pp)
+    b = stage_bounds(topo, L)
+    return max(p for p in range(topo.pp) if b[p] <= l)
 
 
 def tp_owners(h: int, topo: Topology, H: int) -> List[int]:
@@ -121,8 +138,8 @@ def stage_of_rank(r: int, topo: Topology) -> Tuple[int, int]:
 
 def layers_of(r: int, topo: Topology, L: int) -> range:
     p, _ = stage_of_rank(r, topo)
-    per = L // topo.pp
-    return range(p * per, (p + 1) * per)
+    b = stage_bounds(topo, L)
+    return range(b[p], b[p + 1])
 
 
 def heads_of(r: int, topo: Topology, H: int) -> range:

@@ -38,7 +38,7 @@ class RempError(RuntimeError):
 
 
 class Topo(Structure):
-    _fields_ = [("tp", c_int32), ("pp", c_int32)]
+    _fields_ = [("tp", c_int32), ("pp", c_int32), ("layer_starts", POINTER(c_int32))]
 
 
 class Shape(Structure):
@@ -224,13 +224,24 @@ def buffers(entries: Sequence[Optional[Tuple[object, int]]]):
 # the C entry points under their own names
 # ---------------------------------------------------------------------------
 
-def remp_kv_plan(old_topo: Tuple[int, int], new_topo: Tuple[int, int], shape: Tuple[int, ...],
-                 old_tables: HostTables) -> c_void_p:
-    """shape = (num_layers, num_kv_heads, head_dim, elem_bytes, old_block_size, new_block_size)."""
+def _topo(t):
+    """(tp, pp) or (tp, pp, layer_starts) -> (Topo, keep-alive array)."""
+    starts = None
+    if len(t) > 2 and t[2] is not None:
+        starts = _i32(t[2])
+        return Topo(int(t[0]), int(t[1]), starts.ctypes.data_as(POINTER(c_int32))), starts
+    return Topo(int(t[0]), int(t[1]), None), starts
+
+
+def remp_kv_plan(old_topo, new_topo, shape: Tuple[int, ...], old_tables: HostTables) -> c_void_p:
+    """Topologies are (tp, pp) or (tp, pp, layer_starts[pp + 1]);
+    shape = (num_layers, num_kv_heads, head_dim, elem_bytes, old_block_size, new_block_size)."""
     lib = load()
     out = c_void_p()
-    _check(lib.remp_kv_plan(byref(Topo(*old_topo)), byref(Topo(*new_topo)), byref(Shape(*shape)),
-                            byref(old_tables.c), byref(out)), "remp_kv_plan")
+    ot, keep_o = _topo(old_topo)
+    nt, keep_n = _topo(new_topo)
+    _check(lib.remp_kv_plan(byref(ot), byref(nt), byref(Shape(*shape)), byref(old_tables.c), byref(out)),
+           "remp_kv_plan")
     return out
 
 

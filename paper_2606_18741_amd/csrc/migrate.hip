@@ -1047,7 +1047,7 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
         return fail(REMP_E_RANGE, "old_rank " + std::to_string(old_rank) + " outside [0, " +
                                       std::to_string(plan->own_old.world()) + ")");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(plan, src, plan->own_old.layers_per_stage(), plan->shape.old_block_size,
+    if (remp_status st = check_pool(plan, src, plan->own_old.layers_of_rank(old_rank), plan->shape.old_block_size,
                                     "source"))
         return st;
     if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
@@ -1086,7 +1086,7 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
         return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
                                       std::to_string(plan->own_new.world()) + ")");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_per_stage(), plan->shape.new_block_size,
+    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_of_rank(new_rank), plan->shape.new_block_size,
                                     "destination"))
         return st;
     if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
@@ -1123,10 +1123,10 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
     if (rank < 0 || rank >= plan->own_old.world() || rank >= plan->own_new.world())
         return fail(REMP_E_RANGE, "rank " + std::to_string(rank) + " is not a rank of both topologies");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(plan, src, plan->own_old.layers_per_stage(), plan->shape.old_block_size,
+    if (remp_status st = check_pool(plan, src, plan->own_old.layers_of_rank(rank), plan->shape.old_block_size,
                                     "source"))
         return st;
-    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_per_stage(), plan->shape.new_block_size,
+    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_of_rank(rank), plan->shape.new_block_size,
                                     "destination"))
         return st;
     if (src->layout != kLayoutNHD || dst->layout != kLayoutNHD)

@@ -53,13 +53,24 @@ static remp_status check_topo(const remp_topo* t, const char* which, const remp_
     if (!t) return fail(REMP_E_INVALID, std::string(which) + " topology is NULL");
     if (t->tp < 1 || t->pp < 1)
         return fail(REMP_E_INVALID, std::string(which) + " topology needs TP >= 1 and PP >= 1");
+    if (t->pp > s.num_layers)
+        return fail(REMP_E_INVALID, std::string(which) + " topology has more pipeline stages than layers");
     if (s.num_kv_heads % t->tp != 0 && t->tp % s.num_kv_heads != 0)
         return fail(REMP_E_UNSUPPORTED, std::string(which) + " TP=" + std::to_string(t->tp) +
                                             " neither divides nor is a multiple of num_kv_heads=" +
                                             std::to_string(s.num_kv_heads));
+    if (t->layer_starts) {
+        if (t->layer_starts[0] != 0 || t->layer_starts[t->pp] != s.num_layers)
+            return fail(REMP_E_INVALID, std::string(which) + " layer_starts must run from 0 to num_layers");
+        for (int32_t p = 0; p < t->pp; ++p)
+            if (t->layer_starts[p + 1] <= t->layer_starts[p])
+                return fail(REMP_E_INVALID, std::string(which) + " layer_starts must increase (every stage holds a layer)");
+        return REMP_OK;
+    }
     if (s.num_layers % t->pp != 0)
         return fail(REMP_E_UNSUPPORTED, std::string(which) + " PP=" + std::to_string(t->pp) +
-                                            " does not divide num_layers=" + std::to_string(s.num_layers));
+                                            " does not divide num_layers=" + std::to_string(s.num_layers) +
+                                            " (give layer_starts for an uneven split)");
     return REMP_OK;
 }
 
@@ -98,8 +109,16 @@ remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo, c
     p->old_topo = *old_topo;
     p->new_topo = *new_topo;
     p->shape = s;
-    p->own_old = Ownership{old_topo->tp, old_topo->pp, s.num_layers, s.num_kv_heads};
-    p->own_new = Ownership{new_topo->tp, new_topo->pp, s.num_layers, s.num_kv_heads};
+    p->own_old.tp = old_topo->tp;
+    p->own_old.pp = old_topo->pp;
+    p->own_old.L = s.num_layers;
+    p->own_old.H = s.num_kv_heads;
+    p->own_old.set_layers(old_topo->layer_starts);
+    p->own_new.tp = new_topo->tp;
+    p->own_new.pp = new_topo->pp;
+    p->own_new.L = s.num_layers;
+    p->own_new.H = s.num_kv_heads;
+    p->own_new.set_layers(new_topo->layer_starts);
     p->num_seqs = t.num_seqs;
     p->old_num_blocks = t.num_blocks;
 

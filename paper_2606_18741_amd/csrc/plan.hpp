@@ -24,19 +24,30 @@ struct Pair {
 };
 
 // Ownership of one topology (Section 3.4.1).  Layers: stage p holds
-// [p*L/PP, (p+1)*L/PP).  Heads: with TP <= H, tensor rank t holds
+// [starts[p], starts[p+1]) (by default equal ranges [p*L/PP, (p+1)*L/PP)).
+// Heads: with TP <= H, tensor rank t holds
 // [t*H/TP, (t+1)*H/TP); with TP > H (TP a multiple of H, GQA replication) it
 // holds the single head t*H/TP, and each head has TP/H replicas.
 struct Ownership {
-    int32_t tp, pp, L, H;
-    int32_t layers_per_stage() const { return L / pp; }
+    int32_t tp = 1, pp = 1, L = 0, H = 0;
+    std::vector<int32_t> starts;          // [pp + 1] stage boundaries
+    std::vector<int32_t> stage_of_layer;  // [L]
+    void set_layers(const int32_t* layer_starts) {
+        starts.resize(pp + 1);
+        for (int32_t p = 0; p <= pp; ++p)
+            starts[p] = layer_starts ? layer_starts[p] : static_cast<int32_t>(static_cast<int64_t>(p) * L / pp);
+        stage_of_layer.assign(L, 0);
+        for (int32_t p = 0; p < pp; ++p)
+            for (int32_t l = starts[p]; l < starts[p + 1]; ++l) stage_of_layer[l] = p;
+    }
+    int32_t layers_of_rank(int32_t r) const { return starts[stage_of(r) + 1] - starts[stage_of(r)]; }
     int32_t heads_per_rank() const { return tp <= H ? H / tp : 1; }
     int32_t replicas() const { return tp <= H ? 1 : tp / H; }
-    int32_t pp_owner(int32_t l) const { return l / layers_per_stage(); }
+    int32_t pp_owner(int32_t l) const { return stage_of_layer[l]; }
     int32_t rank(int32_t stage, int32_t t) const { return stage * tp + t; }
     int32_t stage_of(int32_t r) const { return r / tp; }
     int32_t tp_of(int32_t r) const { return r % tp; }
-    int32_t first_layer(int32_t r) const { return stage_of(r) * layers_per_stage(); }
+    int32_t first_layer(int32_t r) const { return starts[stage_of(r)]; }
     int32_t first_head_of_tp(int32_t t) const { return static_cast<int32_t>(static_cast<int64_t>(t) * H / tp); }
     int32_t first_head(int32_t r) const { return first_head_of_tp(tp_of(r)); }
     // replica index of tensor rank t among the ranks holding its head (0 without replication)

@@ -11,13 +11,17 @@ from __future__ import annotations
 import numpy as np
 
 
-def explicit_ownership(tp: int, pp: int, L: int, H: int):
+def explicit_ownership(tp: int, pp: int, L: int, H: int, starts=None):
     """List indexed by global rank id: (layers, heads) that rank holds.
 
     Ranks are enumerated stage by stage, tensor rank fastest.  With more
     tensor ranks than heads, each head is repeated on consecutive ranks.
+    `starts` (stage boundaries) splits the layers at the given points.
     """
-    stages = [list(map(int, a)) for a in np.array_split(np.arange(L), pp)]
+    if starts is None:
+        stages = [list(map(int, a)) for a in np.array_split(np.arange(L), pp)]
+    else:
+        stages = [list(map(int, a)) for a in np.split(np.arange(L), list(starts)[1:-1])]
     if tp <= H:
         parts = [list(map(int, a)) for a in np.array_split(np.arange(H), tp)]
     else:
@@ -59,10 +63,11 @@ def slot_list(row, block_size: int):
     return out
 
 
-def migrate(old_pools, new_pools, old_tp, old_pp, new_tp, new_pp, L, H, old_tables, new_tables):
+def migrate(old_pools, new_pools, old_tp, old_pp, new_tp, new_pp, L, H, old_tables, new_tables,
+            old_starts=None, new_starts=None):
     """Write every live element of the new ranks present in new_pools."""
-    own_o = explicit_ownership(old_tp, old_pp, L, H)
-    own_n = explicit_ownership(new_tp, new_pp, L, H)
+    own_o = explicit_ownership(old_tp, old_pp, L, H, old_starts)
+    own_n = explicit_ownership(new_tp, new_pp, L, H, new_starts)
     S = len(old_tables.seq_lens)
     for l in range(L):
         for h in range(H):
@@ -84,10 +89,10 @@ def migrate(old_pools, new_pools, old_tp, old_pp, new_tp, new_pp, L, H, old_tabl
                             new_pools[rn][l][kv, bn, jn, hn, :] = old_pools[ro][l][kv, bo, jo, ho, :]
 
 
-def staging(old_pools, old_tp, old_pp, new_tp, new_pp, L, H, old_tables):
+def staging(old_pools, old_tp, old_pp, new_tp, new_pp, L, H, old_tables, old_starts=None, new_starts=None):
     """{(r, q): flat uint8 buffer} for every pair that exchanges at least one row."""
-    own_o = explicit_ownership(old_tp, old_pp, L, H)
-    own_n = explicit_ownership(new_tp, new_pp, L, H)
+    own_o = explicit_ownership(old_tp, old_pp, L, H, old_starts)
+    own_n = explicit_ownership(new_tp, new_pp, L, H, new_starts)
     S = len(old_tables.seq_lens)
     out = {}
     for r in range(len(own_o)):

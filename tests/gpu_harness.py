@@ -14,7 +14,7 @@ import torch
 
 import paper_2606_18741_amd as rk
 import synthkv
-from hostpools import local_heads, source_stream_rank
+from hostpools import local_heads, source_stream_rank, topo_parts
 
 DEV = "cuda:0"
 STAGING_TAG = 99
@@ -38,8 +38,10 @@ class DeviceTables:
         self.dev = rk.dev_tables(self.lens, self.offs, self.ids)
 
 
-def rank_layers(rank: int, topo: Tuple[int, int], L: int) -> range:
-    tp, pp = topo
+def rank_layers(rank: int, topo, L: int) -> range:
+    tp, pp, starts = topo_parts(topo)
+    if starts is not None:
+        return range(starts[rank // tp], starts[rank // tp + 1])
     per = L // pp
     return range((rank // tp) * per, (rank // tp + 1) * per)
 
@@ -49,7 +51,7 @@ class RankPool:
 
     def __init__(self, w: synthkv.KVWorkload, topo, tables: synthkv.BlockTables, rank: int, fill: str,
                  layers: Optional[Iterable[int]] = None, tag: int = 0, device=DEV):
-        tp, _ = topo
+        tp = topo[0]
         self.rank = rank
         self.layers = rank_layers(rank, topo, w.num_layers)
         H_loc = local_heads(w.num_kv_heads, tp)

@@ -24,9 +24,16 @@ def source_stream_rank(r: int, tp: int, H: int) -> int:
     return r - (r % tp) % rep
 
 
-def rank_layers(r: int, tp: int, pp: int, L: int):
-    per = L // pp
+def topo_parts(topo):
+    """(tp, pp, starts or None) from a (tp, pp) or (tp, pp, starts) topology tuple."""
+    return int(topo[0]), int(topo[1]), (tuple(topo[2]) if len(topo) > 2 and topo[2] is not None else None)
+
+
+def rank_layers(r: int, tp: int, pp: int, L: int, starts=None):
     p = r // tp
+    if starts is not None:
+        return range(starts[p], starts[p + 1])
+    per = L // pp
     return range(p * per, (p + 1) * per)
 
 
@@ -36,13 +43,13 @@ def source_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None, identic
     identical_replicas=False gives every replica its own bytes (to see which
     replica a head was taken from).
     """
-    tp, pp = w.old_topo
+    tp, pp, starts = topo_parts(w.old_topo)
     H_loc = local_heads(w.num_kv_heads, tp)
     dt = synthkv.torch_dtype_for(w.elem_bytes)
     out = {}
     for r in (range(tp * pp) if ranks is None else ranks):
         out[r] = {}
-        for l in rank_layers(r, tp, pp, w.num_layers):
+        for l in rank_layers(r, tp, pp, w.num_layers, starts):
             if layers is not None and l not in layers:
                 continue
             t = torch.empty((2, tables.num_blocks, tables.block_size, H_loc, w.head_dim), dtype=dt)
@@ -55,13 +62,13 @@ def source_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None, identic
 
 def sentinel_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None, tag: int = 0):
     """New-pool pre-fill (sentinel stream) for the given new ranks."""
-    tp, pp = w.new_topo
+    tp, pp, starts = topo_parts(w.new_topo)
     H_loc = local_heads(w.num_kv_heads, tp)
     dt = synthkv.torch_dtype_for(w.elem_bytes)
     out = {}
     for q in (range(tp * pp) if ranks is None else ranks):
         out[q] = {}
-        for l in rank_layers(q, tp, pp, w.num_layers):
+        for l in rank_layers(q, tp, pp, w.num_layers, starts):
             if layers is not None and l not in layers:
                 continue
             t = torch.empty((2, tables.num_blocks, tables.block_size, H_loc, w.head_dim), dtype=dt)

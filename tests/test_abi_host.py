@@ -411,3 +411,24 @@ def test_layout_validation_errors():
         rk.remp_kv_copy_local(p.handle, 0, 0, L, rk.PoolArg(k, v, 64, layout=rk.LAYOUT_HND), s["dev"], s["dst"],
                               rk.HostTables.of(s["new_t"]), s["dev"], s["ws"], s["ws_bytes"], 0)
     assert ei.value.status_name == "REMP_E_UNSUPPORTED"
+
+
+@pytest.mark.parametrize("a,b", [((2, 2, (0, 3, 5)), (1, 1, None)), ((1, 3, (0, 1, 3, 5)), (2, 2, (0, 2, 5))),
+                                 ((8, 2, (0, 4, 5)), (4, 5, None)), ((1, 1, None), (2, 5, (0, 1, 2, 3, 4, 5)))])
+def test_plan_with_explicit_partition(a, b):
+    L, H = 5, 4
+    t = _tables()
+    p = rk.Plan(a, b, (L, H, 8, 2, 16, 16), rk.HostTables.of(t))
+    want = oracle.pair_slices(T(*a), T(*b), L, H)
+    got = {(q.src, q.dst): (list(range(q.layer_begin, q.layer_end)),
+                            list(range(q.head_begin, q.head_begin + q.head_count))) for q in p.pairs}
+    assert got == want
+
+
+def test_plan_partition_errors():
+    t = rk.HostTables.of(_tables())
+    shape = (5, 4, 8, 2, 16, 16)
+    _expect("REMP_E_UNSUPPORTED", rk.Plan, (1, 2), (1, 1), shape, t)               # 5 % 2 without a partition
+    for starts in [(0, 5, 5), (1, 3, 5), (0, 3, 4), (0, 4, 3)]:
+        _expect("REMP_E_INVALID", rk.Plan, (1, 2, starts), (1, 1), shape, t)
+    _expect("REMP_E_INVALID", rk.Plan, (1, 6), (1, 1), (5, 4, 8, 2, 16, 16), t)    # more stages than layers

@@ -470,3 +470,65 @@ def test_layout_positions_by_hand():
     assert k.shape == (2, 3, 2, 4, 8) and v.shape == (2, 3, 16, 4)
     assert k[1, 2, 1, 3, 2] == 0xBEEF and v[1, 2, 10, 3] == 0xCAFE
     assert np.count_nonzero(k) == 1 and np.count_nonzero(v) == 1
+
+
+# ---------------------------------------------------------------------------
+# explicit (uneven) pipeline partitions
+# ---------------------------------------------------------------------------
+
+UNEVEN = [((2, 2, (0, 3, 5)), (1, 1, None), 2, 2),
+          ((1, 3, (0, 1, 3, 5)), (2, 2, (0, 2, 5)), 2, 4),
+          ((2, 1, None), (1, 3, (0, 2, 4, 5)), 4, 2),
+          ((8, 2, (0, 4, 5)), (2, 2, (0, 1, 5)), 2, 2)]      # with replicated heads (H = 4)
+
+
+def _uneven_small(a, b, bs_o, bs_n, seed=17):
+    w = synthkv.KVWorkload(name="uneven", num_layers=5, num_kv_heads=4, head_dim=4, elem_bytes=2, dtype="u16",
+                           old_block_size=bs_o, new_block_size=bs_n, num_seqs=3, length_law=("uniform", 0, 9),
+                           pool_law=("slack", 1.5), old_topo=a, new_topo=b, role="all", seed=seed)
+    return w, synthkv.make_inputs(w)
+
+
+@pytest.mark.parametrize("a,b,bs_o,bs_n", UNEVEN)
+def test_uneven_partition_bruteforce(a, b, bs_o, bs_n):
+    w, inp = _uneven_small(a, b, bs_o, bs_n)
+    L, H = w.num_layers, w.num_kv_heads
+    old = hostpools.source_pools(w, inp.old_tables, identical_replicas=False)
+    new_o = hostpools.sentinel_pools(w, inp.new_tables)
+    new_b = hostpools.copy_pools(new_o)
+    pairs = list(oracle.pair_slices(T(*a), T(*b), L, H))
+    stage = oracle.reshard(old, new_o, T(*a), T(*b), L, H, inp.old_tables, inp.new_tables, pairs=pairs)
+    bruteforce.migrate(old, new_b, a[0], a[1], b[0], b[1], L, H, inp.old_tables, inp.new_tables,
+                       old_starts=a[2], new_starts=b[2])
+    for q in new_o:
+        assert set(new_o[q]) == set(hostpools.rank_layers(q, b[0], b[1], L, b[2]))
+        for l in new_o[q]:
+            np.testing.assert_array_equal(new_o[q][l], new_b[q][l])
+    bst = bruteforce.staging(old, a[0], a[1], b[0], b[1], L, H, inp.old_tables, old_starts=a[2], new_starts=b[2])
+    assert set(bst) == set(pairs)
+    for p in pairs:
+        np.testing.assert_array_equal(oracle.staging_buffer(stage[p]), bst[p])
+
+
+@pytest.mark.parametrize("a,b,bs_o,bs_n", UNEVEN)
+def test_uneven_partition_round_trip(a, b, bs_o, bs_n):
+    w, inp = _uneven_small(a, b, bs_o, bs_n, seed=19)
+    L, H = w.num_layers, w.num_kv_heads
+    old = hostpools.source_pools(w, inp.old_tables)
+    mid = hostpools.sentinel_pools(w, inp.new_tables)
+    oracle.reshard(old, mid, T(*a), T(*b), L, H, inp.old_tables, inp.new_tables)
+    back = hostpools.copy_pools(old)
+    for r in back:
+        for l in back[r]:
+            back[r][l][...] = 0xDEAD
+    oracle.reshard(mid, back, T(*b), T(*a), L, H, inp.new_tables, inp.old_tables)
+    live = _live_mask(inp.old_tables, inp.old_tables.num_blocks, inp.old_tables.block_size)
+    for r in old:
+        for l in old[r]:
+            np.testing.assert_array_equal(back[r][l][:, live], old[r][l][:, live])
+
+
+def test_uneven_partition_rejects_bad_bounds():
+    for starts in [(0, 5), (1, 3, 5), (0, 3, 3), (0, 4, 6)]:
+        with pytest.raises(ValueError):
+            oracle.check_divisible(T(1, 2, starts), 5, 4)

@@ -201,6 +201,12 @@ EDGE = {
     "replicated_tp16_to_tp8pp2": _custom(num_layers=8, num_kv_heads=4, head_dim=64, old_topo=(16, 1),
                                          new_topo=(8, 2), old_block_size=16, new_block_size=32),
     "replicated_keep_local": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(8, 1), new_topo=(4, 2)),
+    # several sources fill each new row with >= 1 KiB shares: unpack writes whole rows
+    "merged_rows_mha": _custom(num_layers=4, num_kv_heads=16, head_dim=128, old_topo=(4, 1), new_topo=(2, 2)),
+    "merged_rows_reblock": _custom(num_layers=4, num_kv_heads=32, head_dim=128, old_topo=(8, 1),
+                                   new_topo=(2, 2), old_block_size=16, new_block_size=32),
+    "short_row_shares_fp8": _custom(num_layers=4, num_kv_heads=32, head_dim=128, elem_bytes=1,
+                                    old_topo=(8, 1), new_topo=(2, 2), old_block_size=16, new_block_size=32),
     # explicit uneven pipeline partitions
     "uneven_pp": _custom(num_layers=5, old_topo=(2, 2, (0, 3, 5)), new_topo=(1, 3, (0, 1, 2, 5))),
     "uneven_to_even": _custom(num_layers=6, old_topo=(1, 4, (0, 1, 3, 4, 6)), new_topo=(2, 2),

@@ -1,11 +1,15 @@
-"""Seeded synthetic inputs for KV-cache migration (shared by the oracle's tests,
-the GPU tests and the benchmark; holds no migration arithmetic)."""
+"""Seeded synthetic inputs for KV-cache migration and the weight-shard rebuild
+(shared by the oracle's tests, the GPU tests and the benchmark; holds no
+migration or slicing arithmetic)."""
 from .configs import KVWorkload, WORKLOADS, TINY, MHA_7B, MHA_13B, GQA_70B, GQA_70B_LONG, reduced
 from .gen import (BlockTables, Inputs, make_inputs, make_tables, seq_lens, tables_from_rows,
                   fill_words_, fill_pool_layer_, fill_sentinel_, words_at, bytes_at, stream_key,
                   torch_dtype_for, numpy_dtype_for, SOURCE, SENTINEL)
+from . import models
+from .models import DecoderSpec, DECODERS, TINY_DECODER, ODD_DECODER, LLAMA2_7B, LLAMA3_70B
 
 __all__ = [
+    "models", "DecoderSpec", "DECODERS", "TINY_DECODER", "ODD_DECODER", "LLAMA2_7B", "LLAMA3_70B",
     "KVWorkload", "WORKLOADS", "TINY", "MHA_7B", "MHA_13B", "GQA_70B", "GQA_70B_LONG", "reduced",
     "BlockTables", "Inputs", "make_inputs", "make_tables", "seq_lens", "tables_from_rows",
     "fill_words_", "fill_pool_layer_", "fill_sentinel_", "words_at", "bytes_at", "stream_key",

@@ -1,0 +1,167 @@
+"""Synthetic decoder models for the weight-shard rebuild: tensor inventories and seeded store contents.
+
+A model here is only a list of parameter tensors with their shapes and the
+tensor-parallel split each one takes (the usual Megatron-style split of a
+Llama-architecture decoder, as vLLM lays it out on the GPU):
+
+    embed_tokens        [V, hidden]      rows split by vocabulary entry     first stage
+    per layer:
+      input_layernorm   [1, hidden]      replicated
+      qkv_proj          q_proj [Hq*D, hidden] | k_proj [Hkv*D, hidden] | v_proj [Hkv*D, hidden],
+                        each split by heads along rows (K and V replicated when TP > Hkv)
+      o_proj            [hidden, Hq*D]   columns split by heads
+      post_attention_layernorm [1, hidden] replicated
+      gate_up_proj      gate_proj [I, hidden] | up_proj [I, hidden], rows split
+      down_proj         [hidden, I]      columns split
+    norm                [1, hidden]      replicated                         last stage
+    lm_head             [V, hidden]      rows split by vocabulary entry     last stage
+
+The store holds every part ("q_proj", "k_proj" ...) whole, as the
+checkpoint does; GPU tensors stack the rank's slices of their parts.  Shapes
+follow the models of the paper's evaluation (Llama2-7B, Llama3-70B); contents
+are seeded hash words, values are never interpreted.  Nothing here slices.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Tuple
+
+import numpy as np
+import torch
+
+from .gen import fill_words_
+
+REPLICATED, SPLIT_ROWS, SPLIT_COLS = 0, 1, 2
+FIRST_STAGE, LAST_STAGE = -1, -2
+WEIGHTS = 0x5745   # stream tag of store contents
+
+
+@dataclass(frozen=True)
+class StorePart:
+    name: str
+    rows: int
+    cols: int
+    split: int
+    units: int
+    key: int          # generator stream of its contents
+
+
+@dataclass(frozen=True)
+class GpuTensor:
+    name: str
+    layer: int                     # >= 0, FIRST_STAGE or LAST_STAGE
+    parts: Tuple[StorePart, ...]   # stacked along rows in the shard
+
+
+@dataclass(frozen=True)
+class DecoderSpec:
+    name: str
+    num_layers: int
+    hidden: int
+    heads: int
+    kv_heads: int
+    head_dim: int
+    intermediate: int
+    vocab: int
+    elem_bytes: int
+    seed: int
+
+    def tensors(self, layers=None) -> List[GpuTensor]:
+        """GPU tensors in load order: embedding, then each layer's, then final norm and LM head.
+        `layers` restricts the decoder layers listed (the embedding / head are always listed)."""
+        H, Hkv, D, h, I, V = self.heads, self.kv_heads, self.head_dim, self.hidden, self.intermediate, self.vocab
+        key = iter(range(1 << 30))
+        out = [GpuTensor("embed_tokens", FIRST_STAGE, (StorePart("embed_tokens", V, h, SPLIT_ROWS, V, next(key)),))]
+        for l in range(self.num_layers):
+            ks = [next(key) for _ in range(9)]
+            if layers is not None and l not in layers:
+                continue
+            out += [
+                GpuTensor(f"layers.{l}.input_layernorm", l,
+                          (StorePart(f"layers.{l}.input_layernorm", 1, h, REPLICATED, 1, ks[0]),)),
+                GpuTensor(f"layers.{l}.qkv_proj", l,
+                          (StorePart(f"layers.{l}.q_proj", H * D, h, SPLIT_ROWS, H, ks[1]),
+                           StorePart(f"layers.{l}.k_proj", Hkv * D, h, SPLIT_ROWS, Hkv, ks[2]),
+                           StorePart(f"layers.{l}.v_proj", Hkv * D, h, SPLIT_ROWS, Hkv, ks[3]))),
+                GpuTensor(f"layers.{l}.o_proj", l, (StorePart(f"layers.{l}.o_proj", h, H * D, SPLIT_COLS, H, ks[4]),)),
+                GpuTensor(f"layers.{l}.post_attention_layernorm", l,
+                          (StorePart(f"layers.{l}.post_attention_layernorm", 1, h, REPLICATED, 1, ks[5]),)),
+                GpuTensor(f"layers.{l}.gate_up_proj", l,
+                          (StorePart(f"layers.{l}.gate_proj", I, h, SPLIT_ROWS, I, ks[6]),
+                           StorePart(f"layers.{l}.up_proj", I, h, SPLIT_ROWS, I, ks[7]))),
+                GpuTensor(f"layers.{l}.down_proj", l, (StorePart(f"layers.{l}.down_proj", h, I, SPLIT_COLS, I, ks[8]),)),
+            ]
+        out += [GpuTensor("norm", LAST_STAGE, (StorePart("norm", 1, h, REPLICATED, 1, next(key)),)),
+                GpuTensor("lm_head", LAST_STAGE, (StorePart("lm_head", V, h, SPLIT_ROWS, V, next(key)),))]
+        return out
+
+    def store_parts(self, layers=None) -> List[StorePart]:
+        return [p for t in self.tensors(layers) for p in t.parts]
+
+    @property
+    def numpy_dtype(self):
+        return {1: np.uint8, 2: np.uint16, 4: np.uint32}[self.elem_bytes]
+
+
+TINY_DECODER = DecoderSpec("tiny", num_layers=4, hidden=64, heads=8, kv_heads=2, head_dim=8, intermediate=96,
+                           vocab=128, elem_bytes=2, seed=11)
+# odd row lengths: every copy falls back to 2-byte vectors
+ODD_DECODER = DecoderSpec("odd", num_layers=3, hidden=36, heads=6, kv_heads=3, head_dim=6, intermediate=30,
+                          vocab=42, elem_bytes=2, seed=12)
+LLAMA2_7B = DecoderSpec("llama2-7b", num_layers=32, hidden=4096, heads=32, kv_heads=32, head_dim=128,
+                        intermediate=11008, vocab=32000, elem_bytes=2, seed=13)
+LLAMA3_70B = DecoderSpec("llama3-70b", num_layers=80, hidden=8192, heads=64, kv_heads=8, head_dim=128,
+                         intermediate=28672, vocab=128256, elem_bytes=2, seed=14)
+DECODERS = {d.name: d for d in (TINY_DECODER, ODD_DECODER, LLAMA2_7B, LLAMA3_70B)}
+
+
+def part_nbytes(spec: DecoderSpec, p: StorePart) -> int:
+    return p.rows * p.cols * spec.elem_bytes
+
+
+def fill_part_(buf: torch.Tensor, spec: DecoderSpec, p: StorePart) -> torch.Tensor:
+    """Fill the flat uint8 tensor `buf` (length >= the part's bytes rounded up to 4) with the part's contents."""
+    n = (part_nbytes(spec, p) + 3) // 4 * 4
+    return fill_words_(buf[:n], spec.seed, WEIGHTS, p.key)
+
+
+def host_store(spec: DecoderSpec, layers=None, pin: bool = False, fill_device=None,
+               chunk_bytes: int = 256 << 20) -> Dict[str, torch.Tensor]:
+    """{part name: flat uint8 host tensor} holding every store part whole.
+
+    pin=True allocates page-locked memory (one allocation per part).  With
+    fill_device (e.g. "cuda") contents are generated there, chunk by chunk, and
+    copied to the host: the same bytes, much faster than on the CPU.
+    """
+    out = {}
+    for p in spec.store_parts(layers):
+        n = part_nbytes(spec, p)
+        padded = (n + 3) // 4 * 4
+        t = torch.empty(padded, dtype=torch.uint8, pin_memory=pin)
+        if fill_device is None:
+            fill_part_(t, spec, p)
+        else:
+            _fill_via_device(t, spec, p, fill_device, chunk_bytes)
+        out[p.name] = t
+    return out
+
+
+def _fill_via_device(t: torch.Tensor, spec: DecoderSpec, p: StorePart, device, chunk_bytes: int) -> None:
+    # word i of the part is hash(i ^ key): generate word ranges on the device and copy them over
+    from .gen import hash_words, stream_key
+    key = stream_key(spec.seed, WEIGHTS, p.key)
+    words = t.view(torch.int32)
+    n = words.numel()
+    step = chunk_bytes // 4
+    for a in range(0, n, step):
+        b = min(n, a + step)
+        idx = torch.arange(a, b, dtype=torch.int64, device=device)
+        words[a:b].copy_(hash_words(idx, key))
+    if str(device).startswith("cuda"):
+        torch.cuda.synchronize()
+
+
+def part_array(spec: DecoderSpec, store: Dict[str, torch.Tensor], p: StorePart) -> np.ndarray:
+    """[rows][cols] numpy view of a store part."""
+    n = part_nbytes(spec, p)
+    return store[p.name][:n].numpy().view(spec.numpy_dtype).reshape(p.rows, p.cols)

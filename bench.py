@@ -28,6 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+PEAK_PCIE_GBS = 64.0   # PCIe Gen5 x16, one direction (32 GT/s x 16 lanes)
 COUNTERS = os.path.join(ROOT, "profiles", "copy_slices_gqa70b_hbm_counters.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_18741_amd", "csrc", "migrate.hip")
 
@@ -47,6 +48,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd", "rocm"],
                     help="physical layout of both pools (hnd and rocm go through the LDS tile kernel)")
+    ap.add_argument("--weight-layers", type=int, default=8,
+                    help="decoder layers of Llama3-70B whose shards new rank 0 rebuilds from the host store "
+                         "(0: skip the weight-shard measurement)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (for counter scaling), then exit")
     return ap.parse_args()
@@ -87,6 +91,87 @@ def copy_calibration(gib: float) -> None:
     ms = e0.elapsed_time(e1) / reps
     print(json.dumps({"copy_bytes_per_launch_read": n, "copy_bytes_per_launch_write": n, "launches": reps,
                       "ms_per_copy": round(ms, 4), "copy_GBps_read_plus_write": round(2 * n / ms / 1e6, 1)}))
+
+
+def bench_weights(args, rk, synthkv, torch, qn, new_topo, kv_step, kv_ms, dev):
+    """Shard rebuild of new rank qn from a page-locked Llama3-70B store (first args.weight_layers
+    layers of its stage plus its non-layer tensors): host-link GB/s alone, then beside the KV step."""
+    from synthkv.models import FIRST_STAGE, LAST_STAGE
+    spec = synthkv.LLAMA3_70B
+    tp, pp = new_topo
+    stage = qn // tp
+    per = spec.num_layers // pp
+    window = range(stage * per, stage * per + min(args.weight_layers, per))
+    # the store holds what this stage reads: its layers' tensors, plus the embedding on the first
+    # stage and the final norm / LM head on the last (the library decides ownership all the same)
+    tensors = [t for t in spec.tensors(window)
+               if t.layer >= 0 or (t.layer == FIRST_STAGE and stage == 0) or (t.layer == LAST_STAGE and stage == pp - 1)]
+    t0 = time.time()
+    store = synthkv.models.host_store(spec, pin=True, fill_device=dev, tensors=tensors)
+    plan = rk.WeightPlan(new_topo, spec.num_layers, spec.elem_bytes,
+                         [(t.layer, [(store[p.name].data_ptr(), p.rows, p.cols, p.split, p.units) for p in t.parts])
+                          for t in tensors])
+    dst = []
+    for i in range(plan.num_tensors):
+        r, c = plan.shard_shape(qn, i)
+        dst.append(torch.empty(r * c * spec.elem_bytes, dtype=torch.uint8, device=dev) if r else None)
+    nbytes = plan.shard_bytes(qn)
+    store_bytes = sum(p.rows * p.cols * spec.elem_bytes for t in tensors for p in t.parts)
+    log(f"weight store ready: {store_bytes / 1e9:.2f} GB page-locked, shard {nbytes / 1e9:.2f} GB "
+        f"({time.time() - t0:.1f}s)")
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+
+    def load(flags):
+        plan.load(qn, dst, side.cuda_stream, flags=flags)
+
+    def alone(flags, reps=3):
+        ts = []
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(side)
+            load(flags)
+            e1.record(side)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return statistics.median(ts[1:])
+
+    def together(flags, k):
+        """k KV steps on the main stream while one load runs on the side stream, started together."""
+        torch.cuda.synchronize()
+        s0 = torch.cuda.Event(enable_timing=True)
+        em, es = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(main)
+        side.wait_event(s0)
+        load(flags)
+        es.record(side)
+        for _ in range(k):
+            kv_step()
+        em.record(main)
+        torch.cuda.synchronize()
+        return s0.elapsed_time(es), s0.elapsed_time(em)
+
+    out = {"model": "llama3-70b", "rank": qn, "topology": f"TP{tp}/PP{pp}",
+           "tensors": f"layers {window.start}-{window.stop - 1}" + (" + embedding" if stage == 0 else "")
+                      + (" + final norm + LM head" if stage == pp - 1 else ""),
+           "store_bytes": store_bytes, "shard_bytes": nbytes, "bound": "host link (PCIe Gen5 x16)",
+           "peak_GBps": PEAK_PCIE_GBS}
+    for name, flags in (("gather_kernel", 0), ("copy_engine", rk.REMP_W_COPY_ENGINE)):
+        ms = alone(flags)
+        k = max(1, round(ms / kv_ms))
+        load_ms, kv_total = together(flags, k)
+        wall = max(load_ms, kv_total)
+        out[name] = {"ms": round(ms, 3), "GBps": round(nbytes / ms / 1e6, 1),
+                     "frac": round(nbytes / ms / 1e6 / PEAK_PCIE_GBS, 4),
+                     "beside_kv": {"kv_steps": k, "kv_ms_alone": round(k * kv_ms, 3),
+                                   "load_ms": round(load_ms, 3), "kv_ms": round(kv_total, 3),
+                                   "wall_ms": round(wall, 3),
+                                   "serial_ms": round(ms + k * kv_ms, 3),
+                                   "ideal_ms": round(max(ms, k * kv_ms), 3)}}
+        log(f"weights ({name}): {ms:.2f} ms alone, {nbytes / ms / 1e6:.1f} GB/s; beside {k} KV steps: "
+            f"load {load_ms:.2f} ms, KV {kv_total:.2f} ms (alone {k * kv_ms:.2f}), wall {wall:.2f} ms")
+    del store, dst
+    return out
 
 
 def main() -> int:
@@ -264,6 +349,10 @@ def main() -> int:
         log(f"local fast path: {ms_local:.3f} ms/step ({ms_per_step / ms_local:.2f}x), "
             f"{local['hbm_GBps']} GB/s of HBM traffic")
 
+    weights = None
+    if args.weight_layers > 0:
+        weights = bench_weights(args, rk, synthkv, torch, qn, w.new_topo, step, ms_per_step, dev)
+
     pack_avg, unpack_avg = statistics.mean(pack_ms), statistics.mean(unpack_ms)
     if pack_avg >= unpack_avg:
         dom, dom_ms, dom_bytes = "pack", pack_avg, 2 * P_pack
@@ -338,6 +427,7 @@ def main() -> int:
         },
         "roofline": roofline,
         "local_fast_path": local,
+        "weights": weights,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

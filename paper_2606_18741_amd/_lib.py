@@ -1,4 +1,4 @@
-"""ctypes binding of libremp_kv.so (include/remp_kv.h): argument marshalling only.
+"""ctypes binding of libremp_kv.so (include/remp_kv.h, include/remp_weights.h): argument marshalling only.
 
 Every step of the migration runs in the library (host planner, HIP kernels);
 this module converts Python values into the C structures and back.  Device
@@ -20,14 +20,20 @@ REMP_OK = 0
 STATUS = {0: "REMP_OK", -1: "REMP_E_INVALID", -2: "REMP_E_UNSUPPORTED", -3: "REMP_E_RANGE",
           -4: "REMP_E_CAPACITY", -5: "REMP_E_ALIGN", -6: "REMP_E_SIZE", -7: "REMP_E_HIP"}
 
-# every symbol include/remp_kv.h declares
+# every symbol include/remp_kv.h and include/remp_weights.h declare
 EXPORTED = (
     "remp_kv_plan", "remp_kv_plan_destroy", "remp_kv_plan_get_info", "remp_kv_plan_get_pair",
     "remp_kv_plan_query", "remp_kv_workspace_bytes", "remp_kv_pack", "remp_kv_unpack", "remp_kv_copy_local",
     "remp_kv_set_trace_events", "remp_status_string", "remp_last_error", "remp_kv_version",
+    "remp_w_plan", "remp_w_plan_destroy", "remp_w_shard_shape", "remp_w_shard_bytes", "remp_w_load",
 )
 
 REMP_KV_SKIP_LOCAL = 1
+
+# remp_weights.h
+REMP_W_REPLICATED, REMP_W_SPLIT_ROWS, REMP_W_SPLIT_COLS = 0, 1, 2
+REMP_W_FIRST_STAGE, REMP_W_LAST_STAGE = -1, -2
+REMP_W_COPY_ENGINE = 1
 
 
 class RempError(RuntimeError):
@@ -65,6 +71,14 @@ LAYOUT_NHD, LAYOUT_HND, LAYOUT_ROCM_SPLIT = 0, 1, 2
 
 class Buffer(Structure):
     _fields_ = [("ptr", c_void_p), ("bytes", c_int64)]
+
+
+class WPart(Structure):
+    _fields_ = [("host", c_void_p), ("rows", c_int64), ("cols", c_int64), ("split", c_int32), ("units", c_int32)]
+
+
+class WTensor(Structure):
+    _fields_ = [("layer", c_int32), ("num_parts", c_int32), ("parts", POINTER(WPart))]
 
 
 class PlanInfo(Structure):
@@ -128,6 +142,17 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.remp_kv_copy_local.restype = st
     lib.remp_kv_set_trace_events.argtypes = [c_void_p, c_void_p]
     lib.remp_kv_set_trace_events.restype = None
+    lib.remp_w_plan.argtypes = [POINTER(Topo), c_int32, c_int32, POINTER(WTensor), c_int32, POINTER(c_void_p)]
+    lib.remp_w_plan.restype = st
+    lib.remp_w_plan_destroy.argtypes = [c_void_p]
+    lib.remp_w_plan_destroy.restype = None
+    lib.remp_w_shard_shape.argtypes = [c_void_p, c_int32, c_int32, POINTER(c_int64), POINTER(c_int64)]
+    lib.remp_w_shard_shape.restype = st
+    lib.remp_w_shard_bytes.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(c_int64)]
+    lib.remp_w_shard_bytes.restype = st
+    lib.remp_w_load.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(c_void_p), ctypes.c_uint32, c_int32,
+                                c_void_p]
+    lib.remp_w_load.restype = st
     lib.remp_status_string.argtypes = [c_int32]
     lib.remp_status_string.restype = c_char_p
     lib.remp_last_error.argtypes = []
@@ -312,6 +337,95 @@ def remp_last_error() -> str:
 
 def remp_kv_version() -> str:
     return load().remp_kv_version().decode()
+
+
+# --- weight shards (remp_weights.h) ---------------------------------------
+
+class WeightTensors:
+    """C arrays of remp_w_tensor / remp_w_part for a list of tensors.
+
+    tensors: sequence of (layer, parts); parts: sequence of
+    (host_address, rows, cols, split, units).  Keeps the arrays alive.
+    """
+
+    def __init__(self, tensors):
+        self.part_arrays = []
+        arr = (WTensor * max(1, len(tensors)))()
+        for i, (layer, parts) in enumerate(tensors):
+            pa = (WPart * len(parts))(*[WPart(int(h) if h else None, int(r), int(c), int(sp), int(u))
+                                        for (h, r, c, sp, u) in parts])
+            self.part_arrays.append(pa)
+            arr[i] = WTensor(int(layer), len(parts), ctypes.cast(pa, POINTER(WPart)))
+        self.array = arr
+        self.count = len(tensors)
+
+
+def remp_w_plan(topo, num_layers: int, elem_bytes: int, tensors: WeightTensors) -> c_void_p:
+    """topo = (tp, pp) or (tp, pp, layer_starts)."""
+    lib = load()
+    out = c_void_p()
+    t, keep = _topo(topo)
+    _check(lib.remp_w_plan(byref(t), int(num_layers), int(elem_bytes), tensors.array, tensors.count, byref(out)),
+           "remp_w_plan")
+    return out
+
+
+def remp_w_plan_destroy(plan) -> None:
+    load().remp_w_plan_destroy(plan)
+
+
+def remp_w_shard_shape(plan, rank: int, tensor: int) -> Tuple[int, int]:
+    r, c = c_int64(), c_int64()
+    _check(load().remp_w_shard_shape(plan, int(rank), int(tensor), byref(r), byref(c)), "remp_w_shard_shape")
+    return int(r.value), int(c.value)
+
+
+def remp_w_shard_bytes(plan, rank: int, tensor_begin: int, tensor_end: int) -> int:
+    b = c_int64()
+    _check(load().remp_w_shard_bytes(plan, int(rank), int(tensor_begin), int(tensor_end), byref(b)),
+           "remp_w_shard_bytes")
+    return int(b.value)
+
+
+def remp_w_load(plan, rank: int, tensor_begin: int, tensor_end: int, dst: Sequence, flags: int,
+                max_workgroups: int, stream) -> None:
+    """dst: one device address (int, tensor or None) per tensor index."""
+    arr = (c_void_p * max(1, len(dst)))(*[_ptr(d) for d in dst])
+    _check(load().remp_w_load(plan, int(rank), int(tensor_begin), int(tensor_end), arr, int(flags),
+                              int(max_workgroups), c_void_p(stream)), "remp_w_load")
+
+
+class WeightPlan:
+    """Owns a remp_w_plan_t; the same calls with the plan bound."""
+
+    def __init__(self, topo, num_layers: int, elem_bytes: int, tensors):
+        self.tensors = tensors if isinstance(tensors, WeightTensors) else WeightTensors(tensors)
+        self.num_tensors = self.tensors.count
+        self.elem_bytes = int(elem_bytes)
+        self.world = int(topo[0]) * int(topo[1])
+        self.handle = remp_w_plan(topo, num_layers, elem_bytes, self.tensors)
+
+    def close(self) -> None:
+        if self.handle:
+            remp_w_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def shard_shape(self, rank: int, tensor: int) -> Tuple[int, int]:
+        return remp_w_shard_shape(self.handle, rank, tensor)
+
+    def shard_bytes(self, rank: int, tensor_begin: int = 0, tensor_end: Optional[int] = None) -> int:
+        return remp_w_shard_bytes(self.handle, rank, tensor_begin, self.num_tensors if tensor_end is None else tensor_end)
+
+    def load(self, rank: int, dst: Sequence, stream, tensor_begin: int = 0, tensor_end: Optional[int] = None,
+             flags: int = 0, max_workgroups: int = 0) -> None:
+        remp_w_load(self.handle, rank, tensor_begin, self.num_tensors if tensor_end is None else tensor_end, dst,
+                    flags, max_workgroups, stream)
 
 
 # ---------------------------------------------------------------------------

@@ -1,4 +1,4 @@
-"""Build libremp_kv.so for gfx950 in-tree with hipcc.
+"""Build libremp_kv.so (KV migration and weight-shard rebuild) for gfx950 in-tree with hipcc.
 
     python paper_2606_18741_amd/build.py      (a plain script: importing the package needs the library)
 """
@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libremp_kv.so")
 
-SOURCES = [os.path.join(CSRC, "plan.cpp"), os.path.join(CSRC, "migrate.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("plan.cpp", "migrate.hip", "weights_plan.cpp", "weights.hip")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -20,6 +20,7 @@
 #include <unordered_set>
 #include <vector>
 
+#include "device_util.hpp"
 #include "plan.hpp"
 
 namespace remp {
@@ -37,27 +38,6 @@ struct BlockDesc {
     int32_t n;
     int32_t seq;
 };
-
-// Division by a runtime constant d for any 32-bit numerator (Granlund and
-// Montgomery, "Division by invariant integers using multiplication", 1994):
-// with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
-// n / d = (mulhi(m, n) + n) >> l, the sum taken in 33 bits.
-struct FastDiv {
-    uint32_t magic;
-    uint32_t shift;
-};
-
-static FastDiv make_fastdiv(uint32_t d) {
-    uint32_t l = 0;
-    while ((uint64_t(1) << l) < d) ++l;
-    uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1;
-    return FastDiv{static_cast<uint32_t>(m), l};
-}
-
-__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t magic, uint32_t shift) {
-    uint64_t t = __umulhi(n, magic);
-    return static_cast<uint32_t>((t + n) >> shift);
-}
 
 constexpr bool kMergeRows = true;    // unpack whole destination rows when several sources fill them
 // ... but only when every source's share of a row is at least this long: with
@@ -230,12 +210,6 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
 // pack / unpack copy
 // ---------------------------------------------------------------------------
 
-template <int VEC> struct VecT;
-template <> struct VecT<16> { typedef unsigned int type __attribute__((ext_vector_type(4))); };
-template <> struct VecT<8> { typedef unsigned int type __attribute__((ext_vector_type(2))); };
-template <> struct VecT<4> { typedef unsigned int type; };
-template <> struct VecT<2> { typedef unsigned short type; };
-template <> struct VecT<1> { typedef unsigned char type; };
 
 template <int VEC, bool PACK, int THREADS, int UNROLL>
 __global__ __launch_bounds__(THREADS) void copy_slices(const CopyArgs args) {
@@ -736,10 +710,6 @@ struct HostSlice {
     uint64_t layer_k = 0, layer_v = 0;   // the layer's storage (no head offset)
 };
 
-static remp_status hip_check(hipError_t e, const char* what) {
-    if (e == hipSuccess) return REMP_OK;
-    return fail(REMP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
-}
 
 // Enqueue expansion of `tables` into the workspace areas at scan_off / desc_off.
 static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables& dt, int32_t bs, int64_t nnz,

@@ -105,7 +105,7 @@ class DecoderSpec:
 
 TINY_DECODER = DecoderSpec("tiny", num_layers=4, hidden=64, heads=8, kv_heads=2, head_dim=8, intermediate=96,
                            vocab=128, elem_bytes=2, seed=11)
-# odd row lengths: every copy falls back to 2-byte vectors
+# row lengths that are not multiples of 16 bytes: copies fall back to narrower vectors
 ODD_DECODER = DecoderSpec("odd", num_layers=3, hidden=36, heads=6, kv_heads=3, head_dim=6, intermediate=30,
                           vocab=42, elem_bytes=2, seed=12)
 LLAMA2_7B = DecoderSpec("llama2-7b", num_layers=32, hidden=4096, heads=32, kv_heads=32, head_dim=128,
@@ -126,15 +126,17 @@ def fill_part_(buf: torch.Tensor, spec: DecoderSpec, p: StorePart) -> torch.Tens
 
 
 def host_store(spec: DecoderSpec, layers=None, pin: bool = False, fill_device=None,
-               chunk_bytes: int = 256 << 20) -> Dict[str, torch.Tensor]:
-    """{part name: flat uint8 host tensor} holding every store part whole.
+               chunk_bytes: int = 256 << 20, tensors=None) -> Dict[str, torch.Tensor]:
+    """{part name: flat uint8 host tensor} holding every store part whole
+    (of `tensors` if given, else of every tensor of `layers`).
 
     pin=True allocates page-locked memory (one allocation per part).  With
     fill_device (e.g. "cuda") contents are generated there, chunk by chunk, and
     copied to the host: the same bytes, much faster than on the CPU.
     """
     out = {}
-    for p in spec.store_parts(layers):
+    parts = spec.store_parts(layers) if tensors is None else [p for t in tensors for p in t.parts]
+    for p in parts:
         n = part_nbytes(spec, p)
         padded = (n + 3) // 4 * 4
         t = torch.empty(padded, dtype=torch.uint8, pin_memory=pin)

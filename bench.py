@@ -399,6 +399,19 @@ def main() -> int:
                          f"and unpack slices of new rank {qn} in those layers ({moved / 1e9:.2f} GB of "
                          f"traffic by the same definition); NumPy, one thread"}
         log(f"oracle: {cpu_s:.1f}s, {cpu_value:.2f} GB/s")
+        # the same oracle and sample, one layer per task on a thread pool the size of this
+        # process's CPU share (NumPy's copies release the interpreter lock)
+        import concurrent.futures
+        threads = len(os.sched_getaffinity(0))
+        t1 = time.perf_counter()
+        with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+            list(ex.map(lambda l: oracle.reshard(old_h, new_h, oracle.Topology(tpo, ppo), oracle.Topology(tpn, ppn),
+                                                 L, H, inp.old_tables, inp.new_tables, layers=[l], pairs=want)
+                        and None, sample))
+        par_s = time.perf_counter() - t1
+        cpu["parallel"] = {"value": round(moved / par_s / 1e9, 3), "unit": "GB/s", "cores": threads,
+                           "seconds": round(par_s, 2), "how": "one layer per task, ThreadPoolExecutor"}
+        log(f"oracle on {threads} threads: {par_s:.1f}s, {moved / par_s / 1e9:.2f} GB/s")
 
     out = {
         "metric": "KV migration GB/s (pack+unpack) and % of MI355X HBM peak, 70B GQA share",

@@ -1,0 +1,43 @@
+"""Seeded random KV-migration configurations for the GPU fuzz tests (inputs only)."""
+from __future__ import annotations
+
+import numpy as np
+
+import synthkv
+
+
+def random_workload(seed: int) -> synthkv.KVWorkload:
+    rng = np.random.default_rng(1000 + seed)
+    L = int(rng.integers(1, 7))
+    H = int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16]))
+    e = int(rng.choice([1, 2, 4]))
+    # head rows of any byte length that is a multiple of 4 (the generator fills 32-bit words)
+    D = int(rng.choice({1: [4, 8, 12, 64, 128], 2: [2, 6, 8, 64, 128], 4: [1, 3, 16, 32]}[e]))
+
+    def topo():
+        tps = [t for t in range(1, 17) if H % t == 0 or t % H == 0]
+        tp = int(rng.choice(tps))
+        pp = int(rng.integers(1, min(L, max(1, 16 // tp), 4) + 1))
+        if pp > 1 and (L % pp or rng.random() < 0.4):
+            cuts = sorted(int(c) for c in rng.choice(np.arange(1, L), pp - 1, replace=False))
+            return (tp, pp, tuple([0] + cuts + [L]))
+        return (tp, pp)
+
+    sizes = [1, 2, 3, 4, 8, 16, 32]
+    if rng.random() < 0.5:
+        pool = ("slack", float(rng.uniform(1.0, 2.0)))
+    else:
+        pool = ("fragmented", float(rng.uniform(0.1, 0.6)))
+    return synthkv.KVWorkload(
+        name=f"fuzz{seed}", num_layers=L, num_kv_heads=H, head_dim=D, elem_bytes=e, dtype="raw",
+        old_block_size=int(rng.choice(sizes)), new_block_size=int(rng.choice(sizes)),
+        num_seqs=int(rng.integers(0, 8)), length_law=("uniform", 0, int(rng.integers(1, 300))),
+        pool_law=pool, old_topo=topo(), new_topo=topo(), role="all", seed=500 + seed)
+
+
+def random_windows(seed: int, L: int):
+    rng = np.random.default_rng(2000 + seed)
+    k = int(rng.integers(0, min(L, 3)))
+    cuts = sorted(int(c) for c in rng.choice(np.arange(1, L), k, replace=False)) if L > 1 and k else []
+    b = [0] + cuts + [L]
+    return list(zip(b[:-1], b[1:]))

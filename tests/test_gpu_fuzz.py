@@ -1,0 +1,29 @@
+"""Seeded random configurations through the GPU path, bit-exact against the oracle.
+
+Shapes, element sizes (1, 2, 4 bytes), head counts with and without
+replication, even and explicit uneven pipeline partitions, block sizes that
+change across the switch, empty and fragmented pools, and layer windows are
+drawn at random (tests/fuzzcases.py); every case runs the staged path over
+random layer windows and the local fast path.
+"""
+from __future__ import annotations
+
+import pytest
+
+import synthkv
+from fuzzcases import random_windows, random_workload
+from test_gpu_parity import check_against_oracle
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 40
+
+
+@pytest.mark.parametrize("seed", range(N_CASES))
+def test_random_configuration(seed):
+    w = random_workload(seed)
+    inp = synthkv.make_inputs(w)
+    check_against_oracle(w, inp, windows=random_windows(seed, w.num_layers),
+                         log_name=f"fuzz{seed} L{w.num_layers} H{w.num_kv_heads} D{w.head_dim} e{w.elem_bytes} "
+                                  f"{w.old_topo}->{w.new_topo} bs {w.old_block_size}->{w.new_block_size}")
+    check_against_oracle(w, inp, local=True, log_name=f"fuzz{seed} local")

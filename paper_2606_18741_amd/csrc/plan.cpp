@@ -43,7 +43,9 @@ WorkspaceLayout workspace_layout(const remp_kv_plan_t& p) {
     w.scan_new = w.scan_old + scan;
     w.desc_old = w.scan_new + scan;
     w.desc_new = w.desc_old + align256(std::max<int64_t>(p.old_live_blocks, 1) * 16);
-    w.total = w.desc_new + align256(std::max<int64_t>(p.new_live_blocks, 1) * 16);
+    w.bucket_new = w.desc_new + align256(std::max<int64_t>(p.new_live_blocks, 1) * 16);
+    w.sorted_new = w.bucket_new + align256(std::max<int64_t>(p.new_live_blocks, 1) * 4);
+    w.total = w.sorted_new + align256(std::max<int64_t>(p.new_live_blocks, 1) * 16);
     return w;
 }
 

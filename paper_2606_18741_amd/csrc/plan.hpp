@@ -88,9 +88,11 @@ int64_t ceil_div(int64_t a, int64_t b);
 // Byte offsets inside the caller's workspace.  Each scan area holds token and
 // block offsets per sequence ([S+1] int32 each); each descriptor area holds
 // one 16-byte descriptor per live block.  Pack uses the old areas, unpack the
-// new ones, the local copy both.
+// new ones, the local copy both.  The new descriptors are also bucket-sorted
+// by physical block (bucket counters, then the sorted copy) so that the
+// unpack side writes the paged pool in ascending address order.
 struct WorkspaceLayout {
-    int64_t scan_old, scan_new, desc_old, desc_new, total;
+    int64_t scan_old, scan_new, desc_old, desc_new, bucket_new, sorted_new, total;
 };
 WorkspaceLayout workspace_layout(const remp_kv_plan_t& p);
 int64_t workspace_bytes(const remp_kv_plan_t& p);

@@ -92,12 +92,22 @@ static_assert(sizeof(CopyArgs) < 4096, "copy kernel arguments must stay below 4 
 // expansion: block tables -> one descriptor per live block
 // ---------------------------------------------------------------------------
 
+// Bucket of a physical block for the descriptor sort of the new tables (see
+// below): nb buckets spread evenly over [0, num_blocks).
+constexpr int kDescsPerBucket = 4;   // buckets = ceil(live blocks / 4): order kept at ~4-block granularity
+
+__device__ __forceinline__ uint32_t block_bucket(int32_t block, int64_t num_blocks, uint32_t nb) {
+    const int64_t b = static_cast<int64_t>(block > 0 ? block : 0) * nb / num_blocks;
+    return static_cast<uint32_t>(b < nb ? b : nb - 1);
+}
+
 // Exclusive prefix sums of tokens and of blocks per sequence (one workgroup,
 // wave64 shuffle scans combined through LDS, carried across chunks of 1024).
 __global__ __launch_bounds__(kScanThreads) void expand_scan(const int32_t* __restrict__ lens, int32_t S,
                                                            int32_t bs, int32_t reset_flag, int32_t* __restrict__ flag,
                                                            int32_t* __restrict__ tok_off,
-                                                           int32_t* __restrict__ blk_off) {
+                                                           int32_t* __restrict__ blk_off,
+                                                           int32_t* __restrict__ bucket, uint32_t nb) {
     __shared__ int64_t wave_tok[kScanThreads / 64];
     __shared__ int64_t wave_blk[kScanThreads / 64];
     __shared__ int64_t carry[2];
@@ -107,6 +117,8 @@ __global__ __launch_bounds__(kScanThreads) void expand_scan(const int32_t* __res
         carry[1] = 0;
         if (reset_flag) *flag = 0;
     }
+    if (bucket)   // counters of the descriptor sort, filled by expand_emit
+        for (uint32_t i = tid; i < nb; i += kScanThreads) bucket[i] = 0;
     __syncthreads();
     bool bad = false;
     for (int32_t base = 0; base < S; base += kScanThreads) {
@@ -183,7 +195,8 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
                                                    const int32_t* __restrict__ tok_off,
                                                    const int32_t* __restrict__ blk_off, int64_t nnz,
                                                    int64_t num_blocks, int64_t total_tokens, int64_t n_desc,
-                                                   BlockDesc* __restrict__ desc, int32_t* __restrict__ flag) {
+                                                   BlockDesc* __restrict__ desc, int32_t* __restrict__ flag,
+                                                   int32_t* __restrict__ bucket, uint32_t nb) {
     const int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (b >= n_desc) return;
     int32_t lo = 0, hi = S;   // last s in [0, S] with blk_off[s] <= b
@@ -211,6 +224,7 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
     }
     if (!ok) *flag = 1;
     desc[b] = d;
+    if (bucket) atomicAdd(&bucket[block_bucket(d.block, num_blocks > 0 ? num_blocks : 1, nb)], 1);
 }
 
 // ---------------------------------------------------------------------------
@@ -222,26 +236,9 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
 // order writes the pool in random 4-64 KiB pieces.  On MI355X random writes
 // cost more than random reads (measured, 4 KiB pieces: 5.6 TB/s scattered
 // writes against 6.1 TB/s scattered reads), so the new descriptors are
-// bucket-sorted by block id first: nb buckets spread evenly over
-// [0, num_blocks), a count, an exclusive scan and a scatter.  Order inside a
-// bucket is whatever the atomics give; every order yields the same bytes.
-constexpr int kDescsPerBucket = 4;   // buckets = ceil(live blocks / 4): order kept at ~4-block granularity
-
-__device__ __forceinline__ uint32_t block_bucket(int32_t block, int64_t num_blocks, uint32_t nb) {
-    const int64_t b = static_cast<int64_t>(block > 0 ? block : 0) * nb / num_blocks;
-    return static_cast<uint32_t>(b < nb ? b : nb - 1);
-}
-
-__global__ __launch_bounds__(256) void sort_clear(int32_t* __restrict__ cnt, uint32_t nb) {
-    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i < nb) cnt[i] = 0;
-}
-
-__global__ __launch_bounds__(256) void sort_count(const BlockDesc* __restrict__ desc, int32_t n, int64_t num_blocks,
-                                                  uint32_t nb, int32_t* __restrict__ cnt) {
-    const int32_t i = static_cast<int32_t>(blockIdx.x * 256 + threadIdx.x);
-    if (i < n) atomicAdd(&cnt[block_bucket(desc[i].block, num_blocks, nb)], 1);
-}
+// bucket-sorted by block id first: the expansion clears and counts the
+// buckets, then an exclusive scan and a scatter.  Order inside a bucket is
+// whatever the atomics give; every order yields the same bytes.
 
 // Exclusive scan of cnt[0, nb) in place (one workgroup, 4 consecutive counters
 // per thread, carried over chunks of 4096).
@@ -831,40 +828,47 @@ struct HostSlice {
 };
 
 
+static uint32_t sort_buckets(int64_t n_desc) {
+    return static_cast<uint32_t>((std::max<int64_t>(n_desc, 1) + kDescsPerBucket - 1) / kDescsPerBucket);
+}
+
 // Enqueue expansion of `tables` into the workspace areas at scan_off / desc_off.
+// With bucket_off >= 0 the expansion also clears and fills the bucket counters
+// of the descriptor sort (new tables only).
 static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables& dt, int32_t bs, int64_t nnz,
                                  int64_t num_blocks, int64_t n_desc, char* ws, int64_t scan_off, int64_t desc_off,
-                                 bool reset_flag, hipStream_t stream) {
+                                 bool reset_flag, hipStream_t stream, int64_t bucket_off = -1) {
+    if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
     int32_t* flag = reinterpret_cast<int32_t*>(ws);
     int32_t* tok_off = reinterpret_cast<int32_t*>(ws + scan_off);
     int32_t* blk_off = tok_off + (p.num_seqs + 1);
     BlockDesc* desc = reinterpret_cast<BlockDesc*>(ws + desc_off);
+    int32_t* bucket = bucket_off >= 0 ? reinterpret_cast<int32_t*>(ws + bucket_off) : nullptr;
+    const uint32_t nb = bucket ? sort_buckets(n_desc) : 0;
     hipLaunchKernelGGL(expand_scan, dim3(1), dim3(kScanThreads), 0, stream, dt.seq_lens, p.num_seqs, bs,
-                       reset_flag ? 1 : 0, flag, tok_off, blk_off);
+                       reset_flag ? 1 : 0, flag, tok_off, blk_off, bucket, nb);
     if (remp_status st = hip_check(hipGetLastError(), "expand_scan launch")) return st;
     if (n_desc > 0) {
         const int64_t blocks = (n_desc + 255) / 256;
         hipLaunchKernelGGL(expand_emit, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, dt.seq_lens,
                            dt.row_offsets, dt.block_ids, p.num_seqs, bs, tok_off, blk_off, nnz, num_blocks,
-                           p.total_tokens, n_desc, desc, flag);
+                           p.total_tokens, n_desc, desc, flag, bucket, nb);
         if (remp_status st = hip_check(hipGetLastError(), "expand_emit launch")) return st;
     }
     return REMP_OK;
 }
 
-// Bucket-sort the n_desc new descriptors at desc_off into sorted_off by physical block.
+// Finish the bucket sort of the n_desc new descriptors at desc_off (counted by
+// the expansion into bucket_off) into sorted_off.
 static remp_status launch_sort_new(int64_t n_desc, int64_t num_blocks, char* ws, int64_t desc_off,
                                    int64_t bucket_off, int64_t sorted_off, hipStream_t stream) {
     if (n_desc <= 0) return REMP_OK;
-    if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
-    const uint32_t nb = static_cast<uint32_t>((n_desc + kDescsPerBucket - 1) / kDescsPerBucket);
+    const uint32_t nb = sort_buckets(n_desc);
     const uint32_t grid = static_cast<uint32_t>((n_desc + 255) / 256);
     const BlockDesc* desc = reinterpret_cast<const BlockDesc*>(ws + desc_off);
     int32_t* cnt = reinterpret_cast<int32_t*>(ws + bucket_off);
     BlockDesc* out = reinterpret_cast<BlockDesc*>(ws + sorted_off);
     const int64_t nblk = num_blocks > 0 ? num_blocks : 1;
-    hipLaunchKernelGGL(sort_clear, dim3(grid), dim3(256), 0, stream, cnt, nb);
-    hipLaunchKernelGGL(sort_count, dim3(grid), dim3(256), 0, stream, desc, static_cast<int32_t>(n_desc), nblk, nb, cnt);
     hipLaunchKernelGGL(sort_scan, dim3(1), dim3(kScanThreads), 0, stream, cnt, nb);
     hipLaunchKernelGGL(sort_scatter, dim3(grid), dim3(256), 0, stream, desc, static_cast<int32_t>(n_desc), nblk, nb,
                        cnt, out);
@@ -1451,7 +1455,7 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
     const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
     if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
-                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream))
+                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream, L.bucket_new))
         return st;
     if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new, L.bucket_new,
                                          L.sorted_new, stream))
@@ -1530,7 +1534,7 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
                                        plan->old_live_blocks, ws, L.scan_old, L.desc_old, true, stream))
         return st;
     if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
-                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, false, stream))
+                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, false, stream, L.bucket_new))
         return st;
     if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new, L.bucket_new,
                                          L.sorted_new, stream))

@@ -226,7 +226,8 @@ def main() -> int:
     dt = synthkv.torch_dtype_for(w.elem_bytes)
 
     def alloc_layer(tables, tp):
-        return torch.empty((2, tables.num_blocks, tables.block_size, H // tp, D), dtype=dt, device=dev)
+        h_loc = H // tp if tp <= H else 1          # with more tensor ranks than KV heads: one replica each
+        return torch.empty((2, tables.num_blocks, tables.block_size, h_loc, D), dtype=dt, device=dev)
 
     # --- inputs ------------------------------------------------------------
     t0 = time.time()
@@ -350,7 +351,7 @@ def main() -> int:
             f"{local['hbm_GBps']} GB/s of HBM traffic")
 
     weights = None
-    if args.weight_layers > 0:
+    if args.weight_layers > 0 and w.name == "gqa70b":     # the weight store models Llama3-70B
         weights = bench_weights(args, rk, synthkv, torch, qn, w.new_topo, step, ms_per_step, dev)
 
     pack_avg, unpack_avg = statistics.mean(pack_ms), statistics.mean(unpack_ms)

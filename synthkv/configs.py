@@ -6,7 +6,9 @@ switch (old TP/PP -> new TP/PP).  Nothing here computes ownership or moves
 data; it only describes inputs.
 
 The shapes follow the models of the paper's evaluation table (Llama2-7B:
-32 layers x 32 KV heads; Llama3-70B: 80 layers x 8 KV heads; head_dim 128).
+32 layers x 32 KV heads; Llama3-70B: 80 layers x 8 KV heads; Qwen3-30B-A3B:
+48 layers x 4 KV heads; DeepSeek-R1-Distill-Qwen-32B: 64 layers x 8 KV heads;
+head_dim 128).
 The 40 x 40 "13B-shaped" workload is a synthetic MHA shape that is not one of
 the paper's models.  The paper does not describe the KV population at switch
 time, so sequence-length laws are synthetic stand-ins: uniform for the small
@@ -106,7 +108,29 @@ GQA_70B_LONG = KVWorkload(
     description="L80 H8 D128 bf16, 8 x 131072 tokens, block size 16 -> 32, TP4/PP2 -> TP8/PP1",
 )
 
-WORKLOADS = {w.name: w for w in (TINY, MHA_7B, MHA_13B, GQA_70B, GQA_70B_LONG)}
+QWEN3_30B = KVWorkload(
+    name="qwen30b",
+    num_layers=48, num_kv_heads=4, head_dim=128, elem_bytes=2, dtype="bf16",
+    old_block_size=16, new_block_size=16,
+    num_seqs=256, length_law=("lognormal", 2048, 0.5, 32768),
+    pool_law=("slack", 1.1),
+    old_topo=(8, 1), new_topo=(4, 2), role=(0, 0), seed=5,
+    description="Qwen3-30B-A3B KV shape: L48 H4 D128 bf16 bs16, 256 seqs lognormal(median 2048, cap 32768), "
+                "TP8/PP1 (each KV head on two ranks) -> TP4/PP2",
+)
+
+DS_32B = KVWorkload(
+    name="ds32b",
+    num_layers=64, num_kv_heads=8, head_dim=128, elem_bytes=2, dtype="bf16",
+    old_block_size=16, new_block_size=16,
+    num_seqs=256, length_law=("lognormal", 2048, 0.5, 32768),
+    pool_law=("slack", 1.1),
+    old_topo=(1, 8), new_topo=(4, 2), role=(0, 0), seed=6,
+    description="DeepSeek-R1-Distill-Qwen-32B KV shape: L64 H8 D128 bf16 bs16, 256 seqs lognormal(median 2048, "
+                "cap 32768), TP1/PP8 -> TP4/PP2",
+)
+
+WORKLOADS = {w.name: w for w in (TINY, MHA_7B, MHA_13B, GQA_70B, GQA_70B_LONG, QWEN3_30B, DS_32B)}
 
 
 def reduced(w: KVWorkload, num_seqs: int = 5, max_len: int = 300, seed_offset: int = 100) -> KVWorkload:

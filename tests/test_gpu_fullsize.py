@@ -26,6 +26,7 @@ from paper_2606_18741_amd import torch_io as tio
 import synthkv
 
 from gpu_harness import DeviceTables, RankPool, log, shape_of
+from hostpools import local_heads
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -35,6 +36,8 @@ FULL = {
     "mha13b": 20,           # layers per window
     "gqa70b": None,
     "gqa70b_long": 20,
+    "qwen30b": None,
+    "ds32b": 16,
 }
 
 
@@ -56,7 +59,7 @@ def _sample_tokens(rng, lens, n):
 def _source_bytes(w, old_topo, old_tables, l, kv, h, s, t):
     """Expected bytes of (layer l, kv, head h, seq s, token t) from the generated source pools."""
     L, H, D, e = w.num_layers, w.num_kv_heads, w.head_dim, w.elem_bytes
-    H_loc = H // old_topo.tp
+    H_loc = local_heads(H, old_topo.tp)
     bs = old_tables.block_size
     out = np.empty((len(l), D * e), np.uint8)
     groups = {}

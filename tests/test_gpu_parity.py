@@ -156,7 +156,7 @@ def test_tiny_all_ranks():
     check_against_oracle(w, synthkv.make_inputs(w))
 
 
-@pytest.mark.parametrize("name", ["mha7b", "mha13b", "gqa70b", "gqa70b_long"])
+@pytest.mark.parametrize("name", ["mha7b", "mha13b", "gqa70b", "gqa70b_long", "qwen30b", "ds32b"])
 def test_reduced_workload_all_ranks(name):
     w = synthkv.reduced(synthkv.WORKLOADS[name], num_seqs=5, max_len=300)
     check_against_oracle(w, synthkv.make_inputs(w))
@@ -291,7 +291,7 @@ def test_mismatched_device_tables_are_contained():
 # local fast path: slices a rank keeps move pool to pool, the rest through staging
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["tiny", "mha7b", "mha13b", "gqa70b", "gqa70b_long"])
+@pytest.mark.parametrize("name", ["tiny", "mha7b", "mha13b", "gqa70b", "gqa70b_long", "qwen30b", "ds32b"])
 def test_local_fast_path(name):
     w = synthkv.WORKLOADS[name]
     if name != "tiny":

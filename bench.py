@@ -49,8 +49,9 @@ def parse():
     ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd", "rocm"],
                     help="physical layout of both pools (hnd and rocm go through the LDS tile kernel)")
     ap.add_argument("--weight-layers", type=int, default=8,
-                    help="decoder layers of Llama3-70B whose shards new rank 0 rebuilds from the host store "
-                         "(0: skip the weight-shard measurement)")
+                    help="decoder layers whose weight shards new rank 0 rebuilds from the host store, for the "
+                         "workloads with a model (gqa70b: Llama3-70B, qwen30b: Qwen3-30B-A3B, ds32b: "
+                         "DeepSeek-R1-Distill-Qwen-32B; 0: skip the weight-shard measurement)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (for counter scaling), then exit")
     return ap.parse_args()
@@ -93,11 +94,14 @@ def copy_calibration(gib: float) -> None:
                       "ms_per_copy": round(ms, 4), "copy_GBps_read_plus_write": round(2 * n / ms / 1e6, 1)}))
 
 
-def bench_weights(args, rk, synthkv, torch, qn, new_topo, kv_step, kv_ms, dev):
-    """Shard rebuild of new rank qn from a page-locked Llama3-70B store (first args.weight_layers
+# KV workload -> the decoder whose weights the same switch rebuilds
+WEIGHT_MODELS = {"gqa70b": "LLAMA3_70B", "qwen30b": "QWEN3_30B_A3B", "ds32b": "QWEN2_32B"}
+
+
+def bench_weights(args, rk, synthkv, torch, qn, new_topo, kv_step, kv_ms, dev, spec):
+    """Shard rebuild of new rank qn from a page-locked store of `spec` (first args.weight_layers
     layers of its stage plus its non-layer tensors): host-link GB/s alone, then beside the KV step."""
     from synthkv.models import FIRST_STAGE, LAST_STAGE
-    spec = synthkv.LLAMA3_70B
     tp, pp = new_topo
     stage = qn // tp
     per = spec.num_layers // pp
@@ -151,7 +155,7 @@ def bench_weights(args, rk, synthkv, torch, qn, new_topo, kv_step, kv_ms, dev):
         torch.cuda.synchronize()
         return s0.elapsed_time(es), s0.elapsed_time(em)
 
-    out = {"model": "llama3-70b", "rank": qn, "topology": f"TP{tp}/PP{pp}",
+    out = {"model": spec.name, "rank": qn, "topology": f"TP{tp}/PP{pp}",
            "tensors": f"layers {window.start}-{window.stop - 1}" + (" + embedding" if stage == 0 else "")
                       + (" + final norm + LM head" if stage == pp - 1 else ""),
            "store_bytes": store_bytes, "shard_bytes": nbytes, "bound": "host link (PCIe Gen5 x16)",
@@ -351,8 +355,10 @@ def main() -> int:
             f"{local['hbm_GBps']} GB/s of HBM traffic")
 
     weights = None
-    if args.weight_layers > 0 and w.name == "gqa70b":     # the weight store models Llama3-70B
-        weights = bench_weights(args, rk, synthkv, torch, qn, w.new_topo, step, ms_per_step, dev)
+    spec = WEIGHT_MODELS.get(w.name)
+    if args.weight_layers > 0 and spec is not None:
+        weights = bench_weights(args, rk, synthkv, torch, qn, w.new_topo, step, ms_per_step, dev,
+                                getattr(synthkv, spec))
 
     pack_avg, unpack_avg = statistics.mean(pack_ms), statistics.mean(unpack_ms)
     if pack_avg >= unpack_avg:

@@ -179,7 +179,6 @@ remp_status remp_w_load(const remp_w_plan_t* plan, int32_t rank, int32_t tensor_
 
     // Validate every destination and source before enqueueing anything.
     std::vector<const char*> src_dev(p.parts.size(), nullptr);
-    uint64_t bits = 16;
     int32_t last_tensor = -1;
     for (size_t k = 0; k < segs.size(); ++k) {
         const WSeg& s = segs[k];
@@ -199,14 +198,11 @@ remp_status remp_w_load(const remp_w_plan_t* plan, int32_t rank, int32_t tensor_
             if (remp_status st = device_view(a.host, a.rows * a.cols * p.elem_bytes, what, &src_dev[s.part]))
                 return st;
         }
-        bits |= reinterpret_cast<uintptr_t>(src_dev[s.part]) | reinterpret_cast<uintptr_t>(a.host) |
-                reinterpret_cast<uintptr_t>(dst[i]) | static_cast<uint64_t>(s.src_off) |
-                static_cast<uint64_t>(s.pitch) | static_cast<uint64_t>(s.width) | static_cast<uint64_t>(s.dst_off);
     }
-    const int vec = static_cast<int>(bits & (~bits + 1));   // widest vector every address and size allows
 
-    std::vector<ReadySeg> ready;
-    ready.reserve(segs.size());
+    // Ready segments, grouped by the widest vector each one's addresses and sizes allow (a short
+    // row-vector part, e.g. a bias, must not narrow the copy of everything else in the call).
+    std::vector<ReadySeg> ready[5];   // vector widths 16, 8, 4, 2, 1
     for (size_t k = 0; k < segs.size(); ++k) {
         const WSeg& s = segs[k];
         ReadySeg r;
@@ -222,42 +218,45 @@ remp_status remp_w_load(const remp_w_plan_t* plan, int32_t rank, int32_t tensor_
             r.pitch = r.width;
             r.rows = 1;
         }
-        if (!(flags & REMP_W_COPY_ENGINE)) {
-            // the gather kernel indexes vectors of one segment with 32 bits: split long ones
-            const int64_t max_vec = (int64_t(1) << 31);
-            if (r.width / vec > max_vec) {
-                if (r.rows != 1)
-                    return fail(REMP_E_UNSUPPORTED, "a strided shard row exceeds 2^31 vectors");
-                const int64_t piece = max_vec * vec;
-                for (int64_t off = 0; off < r.width; off += piece) {
-                    ReadySeg q = r;
-                    q.src_host += off;
-                    q.src_dev += off;
-                    q.dst += off;
-                    q.width = std::min(piece, r.width - off);
-                    q.pitch = q.width;
-                    ready.push_back(q);
-                }
-                continue;
-            }
-            // rows per segment so that rows * vectors-per-row stays below 2^31
-            const int64_t vpr = r.width / vec;
-            const int64_t max_rows = std::max<int64_t>(1, max_vec / vpr);
-            for (int64_t r0 = 0; r0 < r.rows; r0 += max_rows) {
+        if (flags & REMP_W_COPY_ENGINE) {
+            ready[0].push_back(r);
+            continue;
+        }
+        const uint64_t bits = reinterpret_cast<uintptr_t>(r.src_dev) | reinterpret_cast<uintptr_t>(r.dst) |
+                              static_cast<uint64_t>(r.pitch) | static_cast<uint64_t>(r.width) | 16u;
+        const int vec = static_cast<int>(bits & (~bits + 1));
+        std::vector<ReadySeg>& out = ready[vec == 16 ? 0 : vec == 8 ? 1 : vec == 4 ? 2 : vec == 2 ? 3 : 4];
+        // the gather kernel indexes vectors of one segment with 32 bits: split long ones
+        const int64_t max_vec = (int64_t(1) << 31);
+        if (r.width / vec > max_vec) {
+            if (r.rows != 1) return fail(REMP_E_UNSUPPORTED, "a strided shard row exceeds 2^31 vectors");
+            const int64_t piece = max_vec * vec;
+            for (int64_t off = 0; off < r.width; off += piece) {
                 ReadySeg q = r;
-                q.src_host += r0 * r.pitch;
-                q.src_dev += r0 * r.pitch;
-                q.dst += r0 * r.width;
-                q.rows = std::min(max_rows, r.rows - r0);
-                ready.push_back(q);
+                q.src_host += off;
+                q.src_dev += off;
+                q.dst += off;
+                q.width = std::min(piece, r.width - off);
+                q.pitch = q.width;
+                out.push_back(q);
             }
-        } else {
-            ready.push_back(r);
+            continue;
+        }
+        // rows per segment so that rows * vectors-per-row stays below 2^31
+        const int64_t vpr = r.width / vec;
+        const int64_t max_rows = std::max<int64_t>(1, max_vec / vpr);
+        for (int64_t r0 = 0; r0 < r.rows; r0 += max_rows) {
+            ReadySeg q = r;
+            q.src_host += r0 * r.pitch;
+            q.src_dev += r0 * r.pitch;
+            q.dst += r0 * r.width;
+            q.rows = std::min(max_rows, r.rows - r0);
+            out.push_back(q);
         }
     }
 
     if (flags & REMP_W_COPY_ENGINE) {
-        for (const ReadySeg& r : ready) {
+        for (const ReadySeg& r : ready[0]) {
             const hipError_t e = r.rows == 1 ? hipMemcpyAsync(r.dst, r.src_host, r.width, hipMemcpyHostToDevice, stream)
                                              : hipMemcpy2DAsync(r.dst, r.width, r.src_host, r.pitch, r.width, r.rows,
                                                                 hipMemcpyHostToDevice, stream);
@@ -266,13 +265,11 @@ remp_status remp_w_load(const remp_w_plan_t* plan, int32_t rank, int32_t tensor_
         return REMP_OK;
     }
     const int32_t wgs = max_workgroups > 0 ? max_workgroups : kDefaultGatherWgs;
-    switch (vec) {
-        case 16: return launch_gather<16>(ready, wgs, stream);
-        case 8: return launch_gather<8>(ready, wgs, stream);
-        case 4: return launch_gather<4>(ready, wgs, stream);
-        case 2: return launch_gather<2>(ready, wgs, stream);
-        default: return launch_gather<1>(ready, wgs, stream);
-    }
+    if (remp_status st = launch_gather<16>(ready[0], wgs, stream)) return st;
+    if (remp_status st = launch_gather<8>(ready[1], wgs, stream)) return st;
+    if (remp_status st = launch_gather<4>(ready[2], wgs, stream)) return st;
+    if (remp_status st = launch_gather<2>(ready[3], wgs, stream)) return st;
+    return launch_gather<1>(ready[4], wgs, stream);
 }
 
 }  // extern "C"

@@ -16,10 +16,16 @@ Llama-architecture decoder, as vLLM lays it out on the GPU):
     norm                [1, hidden]      replicated                         last stage
     lm_head             [V, hidden]      rows split by vocabulary entry     last stage
 
+Variants: Q/K/V biases (Qwen2, as in DeepSeek-R1-Distill-Qwen-32B) split by
+heads like their weights; per-head Q/K norm weights (Qwen3), replicated; a
+mixture-of-experts MLP (Qwen3-30B-A3B) whose experts are each split by TP
+like a dense MLP, with a replicated router.
+
 The store holds every part ("q_proj", "k_proj" ...) whole, as the
 checkpoint does; GPU tensors stack the rank's slices of their parts.  Shapes
-follow the models of the paper's evaluation (Llama2-7B, Llama3-70B); contents
-are seeded hash words, values are never interpreted.  Nothing here slices.
+follow the models of the paper's evaluation (Llama2-7B, Llama3-70B,
+DeepSeek-R1-Distill-Qwen-32B, Qwen3-30B-A3B); contents are seeded hash words,
+values are never interpreted.  Nothing here slices.
 """
 from __future__ import annotations
 
@@ -65,34 +71,62 @@ class DecoderSpec:
     vocab: int
     elem_bytes: int
     seed: int
+    qkv_bias: bool = False        # Qwen2-style biases on Q, K, V
+    qk_norm: bool = False         # Qwen3-style per-head RMSNorm weights on Q and K
+    num_experts: int = 0          # > 0: a mixture-of-experts MLP of that many experts
+    moe_intermediate: int = 0     # intermediate size of one expert
 
     def tensors(self, layers=None) -> List[GpuTensor]:
         """GPU tensors in load order: embedding, then each layer's, then final norm and LM head.
         `layers` restricts the decoder layers listed (the embedding / head are always listed)."""
         H, Hkv, D, h, I, V = self.heads, self.kv_heads, self.head_dim, self.hidden, self.intermediate, self.vocab
-        key = iter(range(1 << 30))
-        out = [GpuTensor("embed_tokens", FIRST_STAGE, (StorePart("embed_tokens", V, h, SPLIT_ROWS, V, next(key)),))]
+        E, Ie = self.num_experts, self.moe_intermediate
+
+        def part(name, rows, cols, split, units, key):
+            return StorePart(name, rows, cols, split, units, key)
+
+        out = [GpuTensor("embed_tokens", FIRST_STAGE, (part("embed_tokens", V, h, SPLIT_ROWS, V, 1),))]
         for l in range(self.num_layers):
-            ks = [next(key) for _ in range(9)]
             if layers is not None and l not in layers:
                 continue
-            out += [
-                GpuTensor(f"layers.{l}.input_layernorm", l,
-                          (StorePart(f"layers.{l}.input_layernorm", 1, h, REPLICATED, 1, ks[0]),)),
-                GpuTensor(f"layers.{l}.qkv_proj", l,
-                          (StorePart(f"layers.{l}.q_proj", H * D, h, SPLIT_ROWS, H, ks[1]),
-                           StorePart(f"layers.{l}.k_proj", Hkv * D, h, SPLIT_ROWS, Hkv, ks[2]),
-                           StorePart(f"layers.{l}.v_proj", Hkv * D, h, SPLIT_ROWS, Hkv, ks[3]))),
-                GpuTensor(f"layers.{l}.o_proj", l, (StorePart(f"layers.{l}.o_proj", h, H * D, SPLIT_COLS, H, ks[4]),)),
-                GpuTensor(f"layers.{l}.post_attention_layernorm", l,
-                          (StorePart(f"layers.{l}.post_attention_layernorm", 1, h, REPLICATED, 1, ks[5]),)),
-                GpuTensor(f"layers.{l}.gate_up_proj", l,
-                          (StorePart(f"layers.{l}.gate_proj", I, h, SPLIT_ROWS, I, ks[6]),
-                           StorePart(f"layers.{l}.up_proj", I, h, SPLIT_ROWS, I, ks[7]))),
-                GpuTensor(f"layers.{l}.down_proj", l, (StorePart(f"layers.{l}.down_proj", h, I, SPLIT_COLS, I, ks[8]),)),
-            ]
-        out += [GpuTensor("norm", LAST_STAGE, (StorePart("norm", 1, h, REPLICATED, 1, next(key)),)),
-                GpuTensor("lm_head", LAST_STAGE, (StorePart("lm_head", V, h, SPLIT_ROWS, V, next(key)),))]
+            k0 = (l + 1) << 12      # generator streams of layer l's parts: k0 + part number
+            p = f"layers.{l}."
+            t = [GpuTensor(p + "input_layernorm", l, (part(p + "input_layernorm", 1, h, REPLICATED, 1, k0),)),
+                 GpuTensor(p + "qkv_proj", l,
+                           (part(p + "q_proj", H * D, h, SPLIT_ROWS, H, k0 + 1),
+                            part(p + "k_proj", Hkv * D, h, SPLIT_ROWS, Hkv, k0 + 2),
+                            part(p + "v_proj", Hkv * D, h, SPLIT_ROWS, Hkv, k0 + 3)))]
+            if self.qkv_bias:   # biases as column vectors: they stack like the weights' rows
+                t.append(GpuTensor(p + "qkv_bias", l,
+                                   (part(p + "q_bias", H * D, 1, SPLIT_ROWS, H, k0 + 4),
+                                    part(p + "k_bias", Hkv * D, 1, SPLIT_ROWS, Hkv, k0 + 5),
+                                    part(p + "v_bias", Hkv * D, 1, SPLIT_ROWS, Hkv, k0 + 6))))
+            if self.qk_norm:
+                t.append(GpuTensor(p + "q_norm", l, (part(p + "q_norm", 1, D, REPLICATED, 1, k0 + 7),)))
+                t.append(GpuTensor(p + "k_norm", l, (part(p + "k_norm", 1, D, REPLICATED, 1, k0 + 8),)))
+            t.append(GpuTensor(p + "o_proj", l, (part(p + "o_proj", h, H * D, SPLIT_COLS, H, k0 + 9),)))
+            t.append(GpuTensor(p + "post_attention_layernorm", l,
+                               (part(p + "post_attention_layernorm", 1, h, REPLICATED, 1, k0 + 10),)))
+            if E:
+                # experts under tensor parallelism: every expert's gate / up rows and down columns split by TP;
+                # the router is replicated.  Fused as [expert][gate | up][rows][hidden] and [expert][hidden][cols].
+                t.append(GpuTensor(p + "router", l, (part(p + "router", E, h, REPLICATED, 1, k0 + 11),)))
+                w13 = []
+                for e in range(E):
+                    w13.append(part(p + f"experts.{e}.gate_proj", Ie, h, SPLIT_ROWS, Ie, k0 + 16 + 3 * e))
+                    w13.append(part(p + f"experts.{e}.up_proj", Ie, h, SPLIT_ROWS, Ie, k0 + 17 + 3 * e))
+                t.append(GpuTensor(p + "experts.w13", l, tuple(w13)))
+                t.append(GpuTensor(p + "experts.w2", l,
+                                   tuple(part(p + f"experts.{e}.down_proj", h, Ie, SPLIT_COLS, Ie, k0 + 18 + 3 * e)
+                                         for e in range(E))))
+            else:
+                t.append(GpuTensor(p + "gate_up_proj", l,
+                                   (part(p + "gate_proj", I, h, SPLIT_ROWS, I, k0 + 12),
+                                    part(p + "up_proj", I, h, SPLIT_ROWS, I, k0 + 13))))
+                t.append(GpuTensor(p + "down_proj", l, (part(p + "down_proj", h, I, SPLIT_COLS, I, k0 + 14),)))
+            out += t
+        out += [GpuTensor("norm", LAST_STAGE, (part("norm", 1, h, REPLICATED, 1, 2),)),
+                GpuTensor("lm_head", LAST_STAGE, (part("lm_head", V, h, SPLIT_ROWS, V, 3),))]
         return out
 
     def store_parts(self, layers=None) -> List[StorePart]:
@@ -108,11 +142,23 @@ TINY_DECODER = DecoderSpec("tiny", num_layers=4, hidden=64, heads=8, kv_heads=2,
 # row lengths that are not multiples of 16 bytes: copies fall back to narrower vectors
 ODD_DECODER = DecoderSpec("odd", num_layers=3, hidden=36, heads=6, kv_heads=3, head_dim=6, intermediate=30,
                           vocab=42, elem_bytes=2, seed=12)
+TINY_BIAS = DecoderSpec("tiny-bias", num_layers=2, hidden=32, heads=4, kv_heads=2, head_dim=8, intermediate=48,
+                        vocab=64, elem_bytes=2, seed=15, qkv_bias=True)
+TINY_MOE = DecoderSpec("tiny-moe", num_layers=2, hidden=32, heads=8, kv_heads=2, head_dim=4, intermediate=0,
+                       vocab=64, elem_bytes=2, seed=16, qk_norm=True, num_experts=4, moe_intermediate=16)
 LLAMA2_7B = DecoderSpec("llama2-7b", num_layers=32, hidden=4096, heads=32, kv_heads=32, head_dim=128,
                         intermediate=11008, vocab=32000, elem_bytes=2, seed=13)
 LLAMA3_70B = DecoderSpec("llama3-70b", num_layers=80, hidden=8192, heads=64, kv_heads=8, head_dim=128,
                          intermediate=28672, vocab=128256, elem_bytes=2, seed=14)
-DECODERS = {d.name: d for d in (TINY_DECODER, ODD_DECODER, LLAMA2_7B, LLAMA3_70B)}
+# DeepSeek-R1-Distill-Qwen-32B (Qwen2 architecture: biases on Q, K, V)
+QWEN2_32B = DecoderSpec("deepseek-r1-distill-qwen-32b", num_layers=64, hidden=5120, heads=40, kv_heads=8,
+                        head_dim=128, intermediate=27648, vocab=152064, elem_bytes=2, seed=17, qkv_bias=True)
+# Qwen3-30B-A3B (mixture of 128 experts, per-head Q/K norms)
+QWEN3_30B_A3B = DecoderSpec("qwen3-30b-a3b", num_layers=48, hidden=2048, heads=32, kv_heads=4, head_dim=128,
+                            intermediate=0, vocab=151936, elem_bytes=2, seed=18, qk_norm=True, num_experts=128,
+                            moe_intermediate=768)
+DECODERS = {d.name: d for d in (TINY_DECODER, ODD_DECODER, TINY_BIAS, TINY_MOE, LLAMA2_7B, LLAMA3_70B, QWEN2_32B,
+                                QWEN3_30B_A3B)}
 
 
 def part_nbytes(spec: DecoderSpec, p: StorePart) -> int:

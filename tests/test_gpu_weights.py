@@ -112,6 +112,28 @@ def test_element_sizes(elem_bytes):
     run_case(spec, (8, 1), flags=_rk().REMP_W_COPY_ENGINE)
 
 
+@pytest.mark.parametrize("spec_name,topo", [("tiny-bias", (2, 2)), ("tiny-bias", (8, 1)), ("tiny-moe", (4, 2)),
+                                            ("tiny-moe", (8, 1)), ("tiny-moe", (2, 2, (0, 1, 2)))])
+def test_model_variants(spec_name, topo):
+    """Q/K/V biases, per-head Q/K norms and mixture-of-experts tensors (hundreds of parts per tensor)."""
+    run_case(synthkv.DECODERS[spec_name], topo)
+    run_case(synthkv.DECODERS[spec_name], topo, flags=_rk().REMP_W_COPY_ENGINE, ranks=[0])
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("spec_name,topo,ranks", [("deepseek-r1-distill-qwen-32b", (4, 2), [0, 5]),
+                                                  ("qwen3-30b-a3b", (4, 2), [0, 7]),
+                                                  ("qwen3-30b-a3b", (8, 1), [6])])
+def test_real_shapes_one_layer(spec_name, topo, ranks):
+    """Real shapes of the paper's other evaluation models: layer 0 (with its 128 experts for Qwen3-30B-A3B),
+    embedding and LM head, whole shards compared."""
+    spec = synthkv.DECODERS[spec_name]
+    layers = range(1)
+    log(f"[weights] filling the {spec.name} store (layer 0, embedding, LM head) in page-locked memory")
+    store = synthkv.models.host_store(spec, layers, pin=True, fill_device=DEV)
+    run_case(spec, topo, ranks=ranks, store=store, layers=layers)
+
+
 @pytest.mark.parametrize("max_wgs", [1, 3, 1000])
 def test_grid_caps(max_wgs):
     run_case(synthkv.TINY_DECODER, (2, 2), max_wgs=max_wgs)

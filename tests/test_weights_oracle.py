@@ -6,8 +6,10 @@
   replicated KV heads included;
 * the mathematics of tensor parallelism: with float64 weights, a decoder
   layer computed shard by shard (grouped-query attention on each rank's local
-  heads, row-parallel partial sums, vocabulary-parallel embedding lookups)
-  equals the same layer computed with the full weights;
+  heads with Q/K/V biases and per-head Q/K norms where the model has them,
+  row-parallel partial sums, every expert of a mixture of experts,
+  vocabulary-parallel embedding lookups) equals the same layer computed with
+  the full weights;
 * planted mistakes in the oracle, each of which one of the above catches.
 """
 from __future__ import annotations
@@ -51,6 +53,8 @@ TOPOS = {
     "tiny": [(1, 1), (2, 1), (4, 1), (8, 1), (1, 2), (2, 2), (4, 2), (8, 2), (2, 4), (1, 4),
              (2, 2, (0, 1, 4)), (4, 3, (0, 2, 3, 4)), (8, 2, (0, 3, 4))],
     "odd": [(1, 1), (3, 1), (6, 1), (1, 3), (3, 3), (6, 3), (3, 2, (0, 2, 3)), (6, 2, (0, 1, 3))],
+    "tiny-bias": [(1, 1), (2, 2), (4, 1), (8, 1)],
+    "tiny-moe": [(1, 1), (2, 2), (4, 1), (8, 2)],
 }
 
 
@@ -125,49 +129,56 @@ def _attention(q, k, v, heads, kv_heads, D):
     return out.reshape(T, heads * D)
 
 
-def _layer_full(tensors, l_index, x, spec):
-    """One decoder layer (without norms' arithmetic) and the embedding / LM head, full weights."""
-    emb, n_in, qkv, o, n_post, gu, down = (tensors[0],) + tuple(tensors[1 + 6 * l_index + j] for j in range(6))
-    Wq, Wk, Wv = (qkv[1][j][0] for j in range(3))
-    Wo = o[1][0][0]
-    Wg, Wu = gu[1][0][0], gu[1][1][0]
-    Wd = down[1][0][0]
-    attn = _attention(x @ Wq.T, x @ Wk.T, x @ Wv.T, spec.heads, spec.kv_heads, spec.head_dim)
-    h1 = attn @ Wo.T
-    h2 = (_silu(x @ Wg.T) * (x @ Wu.T)) @ Wd.T
-    return h1, h2, n_in[1][0][0], n_post[1][0][0]
+def _rms(z, w):
+    return z / np.sqrt((z * z).mean(axis=-1, keepdims=True) + 1e-6) * w
 
 
-def _layer_sharded(tensors, l_index, x, spec, tp):
-    """The same layer computed rank by rank from the oracle's shards, then combined."""
-    H, Hkv, D, I = spec.heads, spec.kv_heads, spec.head_dim, spec.intermediate
-    topo = Topology(tp, 1)
-    L = spec.num_layers
-    qkv_i, o_i, gu_i, down_i = 2 + 6 * l_index, 3 + 6 * l_index, 5 + 6 * l_index, 6 + 6 * l_index
-    n_in_i, n_post_i = 1 + 6 * l_index, 4 + 6 * l_index
+def _attn_in(y, nq, nkv, D, qn=None, kn=None):
+    """Split a fused Q|K|V projection output; apply per-head Q/K norms when given."""
+    T = y.shape[0]
+    q, k, v = y[:, :nq * D], y[:, nq * D:(nq + nkv) * D], y[:, (nq + nkv) * D:]
+    assert v.shape[1] == nkv * D
+    if qn is not None:
+        q = _rms(q.reshape(T, nq, D), qn.reshape(-1)).reshape(T, nq * D)
+        k = _rms(k.reshape(T, nkv, D), kn.reshape(-1)).reshape(T, nkv * D)
+    return q, k, v
+
+
+def _layer(get, x, spec, l, tp):
+    """Attention and MLP outputs of layer l, from the GPU tensors `get(name)` of one tensor rank
+    (tp = 1: the full weights).  Row-parallel outputs are partial sums over ranks."""
+    H, Hkv, D = spec.heads, spec.kv_heads, spec.head_dim
     h_loc = H // tp
     kv_loc = Hkv // tp if tp <= Hkv else 1
-    h1 = np.zeros((x.shape[0], spec.hidden))
-    h2 = np.zeros((x.shape[0], spec.hidden))
-    norms = []
-    for t in range(tp):
-        s = ow.rank_shards(tensors, topo, L, t)
-        y = x @ s[qkv_i].T
-        q, k, v = y[:, :h_loc * D], y[:, h_loc * D:(h_loc + kv_loc) * D], y[:, (h_loc + kv_loc) * D:]
-        assert v.shape[1] == kv_loc * D
-        attn_t = _attention(q, k, v, h_loc, kv_loc, D)
-        h1 += attn_t @ s[o_i].T                       # row-parallel: partial sums
-        gu = x @ s[gu_i].T
-        i_loc = I // tp
-        h2 += (_silu(gu[:, :i_loc]) * gu[:, i_loc:]) @ s[down_i].T
-        norms.append((s[n_in_i], s[n_post_i]))
-    return h1, h2, norms
+    p = f"layers.{l}."
+    y = x @ get(p + "qkv_proj").T
+    if spec.qkv_bias:
+        y = y + get(p + "qkv_bias").reshape(-1)
+    qn = get(p + "q_norm") if spec.qk_norm else None
+    kn = get(p + "k_norm") if spec.qk_norm else None
+    q, k, v = _attn_in(y, h_loc, kv_loc, D, qn, kn)
+    attn = _attention(q, k, v, h_loc, kv_loc, D) @ get(p + "o_proj").T
+    if spec.num_experts:
+        E, h = spec.num_experts, spec.hidden
+        i_loc = spec.moe_intermediate // tp
+        logits = x @ get(p + "router").T
+        g = np.exp(logits - logits.max(axis=1, keepdims=True))
+        g /= g.sum(axis=1, keepdims=True)            # every expert weighted (a dense mixture checks them all)
+        w13, w2 = get(p + "experts.w13"), get(p + "experts.w2")
+        mlp = np.zeros((x.shape[0], h))
+        for e in range(E):
+            gu = x @ w13[e * 2 * i_loc:(e + 1) * 2 * i_loc].T
+            mlp += g[:, e:e + 1] * ((_silu(gu[:, :i_loc]) * gu[:, i_loc:]) @ w2[e * h:(e + 1) * h].T)
+    else:
+        i_loc = spec.intermediate // tp
+        gu = x @ get(p + "gate_up_proj").T
+        mlp = (_silu(gu[:, :i_loc]) * gu[:, i_loc:]) @ get(p + "down_proj").T
+    return attn, mlp
 
 
 @pytest.mark.parametrize("tp", [1, 2, 4, 8])
 def test_sharded_layer_equals_full_layer(tp):
-    spec = synthkv.TINY_DECODER
-    _check_tp_math(spec, tp)
+    _check_tp_math(synthkv.TINY_DECODER, tp)
 
 
 @pytest.mark.parametrize("tp", [3, 6])
@@ -175,34 +186,51 @@ def test_sharded_layer_equals_full_layer_odd(tp):
     _check_tp_math(synthkv.ODD_DECODER, tp)
 
 
+@pytest.mark.parametrize("spec_name,tp", [("tiny-bias", 2), ("tiny-bias", 4), ("tiny-moe", 2), ("tiny-moe", 4),
+                                          ("tiny-moe", 8)])
+def test_sharded_layer_equals_full_layer_variants(spec_name, tp):
+    """Q/K/V biases (Qwen2), per-head Q/K norms and a mixture of experts (Qwen3 MoE)."""
+    _check_tp_math(synthkv.DECODERS[spec_name], tp)
+
+
 def _check_tp_math(spec, tp):
     rng = np.random.default_rng(100 + tp)
     tensors = _float_decoder(spec, rng)
+    names = [t.name for t in spec.tensors()]
+    index = {n: i for i, n in enumerate(names)}
+    # the full-weight GPU tensor: its parts, whole, stacked along rows
+    full = {n: np.concatenate([a for (a, _, _) in tensors[i][1]], axis=0) for n, i in index.items()}
+    topo = Topology(tp, 1)
+    L = spec.num_layers
+    shards = [ow.rank_shards(tensors, topo, L, t) for t in range(tp)]
     T = 5
     x = rng.standard_normal((T, spec.hidden))
-    for l_index in range(spec.num_layers):
-        f1, f2, n_in, n_post = _layer_full(tensors, l_index, x, spec)
-        s1, s2, norms = _layer_sharded(tensors, l_index, x, spec, tp)
-        np.testing.assert_allclose(s1, f1, rtol=1e-9, atol=1e-9)
-        np.testing.assert_allclose(s2, f2, rtol=1e-9, atol=1e-9)
-        for a, b in norms:
-            np.testing.assert_array_equal(a, n_in)
-            np.testing.assert_array_equal(b, n_post)
+    for l in range(L):
+        f_attn, f_mlp = _layer(lambda n: full[n], x, spec, l, 1)
+        s_attn = np.zeros_like(f_attn)
+        s_mlp = np.zeros_like(f_mlp)
+        for t in range(tp):
+            a, m = _layer(lambda n: shards[t][index[n]], x, spec, l, tp)
+            s_attn += a
+            s_mlp += m
+        np.testing.assert_allclose(s_attn, f_attn, rtol=1e-9, atol=1e-9)
+        np.testing.assert_allclose(s_mlp, f_mlp, rtol=1e-9, atol=1e-9)
+        for n in ("input_layernorm", "post_attention_layernorm", "q_norm", "k_norm", "router"):
+            if f"layers.{l}.{n}" in index:
+                for t in range(tp):
+                    np.testing.assert_array_equal(shards[t][index[f"layers.{l}.{n}"]], full[f"layers.{l}.{n}"])
     # vocabulary-parallel embedding (masked lookups summed) and LM head (logits concatenated)
     V = spec.vocab
-    topo = Topology(tp, 1)
-    E = tensors[0][1][0][0]
-    W = tensors[-1][1][0][0]
+    E, W = full["embed_tokens"], full["lm_head"]
     ids = rng.integers(0, V, size=17)
     emb = np.zeros((ids.size, spec.hidden))
     logits = []
     hdn = rng.standard_normal((3, spec.hidden))
     for t in range(tp):
-        s = ow.rank_shards(tensors, topo, spec.num_layers, t)
         lo = t * (V // tp)
         mine = (ids >= lo) & (ids < lo + V // tp)
-        emb[mine] += s[0][ids[mine] - lo]
-        logits.append(hdn @ s[len(tensors) - 1].T)
+        emb[mine] += shards[t][index["embed_tokens"]][ids[mine] - lo]
+        logits.append(hdn @ shards[t][index["lm_head"]].T)
     np.testing.assert_array_equal(emb, E[ids])
     np.testing.assert_allclose(np.concatenate(logits, axis=1), hdn @ W.T, rtol=1e-12, atol=1e-12)
 

@@ -325,7 +325,7 @@ def main() -> int:
     # --- the same share with the local fast path (slices old rank ro keeps as new
     # rank qn go pool to pool; the rest through staging), timed the same way
     local = None
-    if ro == qn and (ro, qn) in pair_info and layout == rk.LAYOUT_NHD:
+    if ro == qn and (ro, qn) in pair_info:
         P_local = pair_info[(ro, qn)].staging_bytes
         st_out_r = tio.staging_args({k: v for k, v in staging.items() if k[0] == ro and k[1] != ro}, ro, W_new, True)
         st_in_r = tio.staging_args({k: v for k, v in staging.items() if k[1] == qn and k[0] != qn}, qn, W_old, False)

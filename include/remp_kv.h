@@ -260,8 +260,10 @@ REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank
  * pool, addressed by new_tables), without staging.  Together with pack and
  * unpack called with REMP_KV_SKIP_LOCAL this yields the same new pool as a
  * staged migration while moving the local share once instead of twice.
- * rank must exist in both topologies; both pools must be NHD
- * (REMP_E_UNSUPPORTED otherwise).  src and dst storage must not overlap
+ * rank must exist in both topologies.  The two pools may have any layouts
+ * (for HND or ROCM_SPLIT pools head tiles go through LDS; those layouts need
+ * head_dim * elem_bytes % 16 == 0 and the new block size at most 1024,
+ * REMP_E_UNSUPPORTED otherwise).  src and dst storage must not overlap
  * (checked per layer, REMP_E_INVALID).  new_tables are validated as in
  * remp_kv_unpack.  old_tables / new_dev_tables: device copies of the tables.
  * The workspace is the one remp_kv_workspace_bytes sizes; nothing is enqueued

@@ -703,6 +703,224 @@ __global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) 
 
 
 // ---------------------------------------------------------------------------
+// local copy between pools of any layouts, one head tile at a time through LDS
+// ---------------------------------------------------------------------------
+//
+// A unit is one (new block, K or V, head of the slice) tile.  The prologue
+// resolves each of its rows to the old (block, slot) through the old
+// descriptors; phase 1 reads every live row's head vectors from the old pool
+// in its layout into LDS (token-major); phase 2 writes the tile into the new
+// pool in its layout, live slots only.  NHD rows on either side are read or
+// written as 16-byte vectors of the row; the ROCm V layout, where a token's
+// elements of one head lie block_size elements apart, is read element-wise.
+
+constexpr int kMaxLocalTileItems = 48;
+
+struct LocalTileItem {
+    uint64_t src_k, src_v;   // old storage of the layer at the slice's first head (block 0)
+    uint64_t dst_k, dst_v;   // new storage of the layer at the slice's first head (block 0)
+    int32_t heads;           // heads in the slice
+    int32_t pad;
+};
+
+struct LocalTileArgs {
+    const BlockDesc* new_desc;
+    const BlockDesc* old_desc;
+    const int32_t* tok_off;       // first token of each sequence on the token axis
+    const int32_t* old_blk_off;   // first old descriptor of each sequence
+    int32_t* flag;
+    int64_t old_block_stride, new_block_stride;   // bytes per block (all local heads)
+    int32_t n_new_desc, n_old_desc;
+    int32_t tiles_per_wg;
+    int32_t old_block_size, new_block_size;
+    int32_t head_bytes, elem_bytes;
+    int32_t old_layout, new_layout;
+    int32_t old_row_stride, new_row_stride;       // NHD: bytes per token row of all local heads
+    int32_t old_head_step, new_head_step;         // bytes from one head's data to the next at block 0
+    int32_t lds_row;                              // head_bytes + 16
+    uint32_t vph_magic, vph_shift;                // division by vectors per head row
+    uint32_t rows_magic, rows_shift;              // division by new_block_size * vectors per head row
+    uint32_t bn_magic, bn_shift;                  // division by the new block size
+    LocalTileItem items[kMaxLocalTileItems];
+};
+static_assert(sizeof(LocalTileArgs) < 4096, "local tile kernel arguments must stay below 4 KiB");
+
+__global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTileArgs a) {
+    typedef unsigned int V4 __attribute__((ext_vector_type(4)));
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+    __shared__ uint64_t s_dst[kMaxUnitsPerWg];
+    __shared__ int32_t s_n[kMaxUnitsPerWg];
+    __shared__ int32_t s_kv[kMaxUnitsPerWg];
+    __shared__ uint64_t s_src[kMaxLocalRows];    // old tile (block, head) base of each (unit, row), 0: none
+    __shared__ int32_t s_slot[kMaxLocalRows];
+
+    const LocalTileItem& it = a.items[blockIdx.y];
+    const int32_t hc = it.heads;
+    const int64_t ntiles = static_cast<int64_t>(a.n_new_desc) * 2 * hc;
+    const int64_t g0 = static_cast<int64_t>(blockIdx.x) * a.tiles_per_wg;
+    if (g0 >= ntiles) return;
+    const int32_t nt = static_cast<int32_t>(min(static_cast<int64_t>(a.tiles_per_wg), ntiles - g0));
+    const int tid = threadIdx.x;
+    const int32_t bn = a.new_block_size, bo = a.old_block_size, hb = a.head_bytes, eb = a.elem_bytes;
+
+    for (int i = tid; i < nt; i += kTileThreads) {
+        const int64_t g = g0 + i;
+        const int64_t d = g / (2 * hc);
+        const int32_t r = static_cast<int32_t>(g - d * 2 * hc);
+        const int32_t kv = r / hc, j = r - (r / hc) * hc;
+        const BlockDesc nd = a.new_desc[d];
+        s_dst[i] = (kv ? it.dst_v : it.dst_k) + static_cast<uint64_t>(nd.block) * a.new_block_stride +
+                   static_cast<uint64_t>(j) * a.new_head_step;
+        s_n[i] = nd.n;
+        s_kv[i] = kv;
+    }
+    for (int x = tid; x < nt * bn; x += kTileThreads) {
+        const int32_t i = x / bn, r = x - (x / bn) * bn;
+        const int64_t g = g0 + i;
+        const int64_t d = g / (2 * hc);
+        const int32_t rr = static_cast<int32_t>(g - d * 2 * hc);
+        const int32_t kv = rr / hc, j = rr - (rr / hc) * hc;
+        const BlockDesc nd = a.new_desc[d];
+        uint64_t base = 0;
+        int32_t slot = 0;
+        if (r < nd.n) {
+            const int32_t t = nd.tok - a.tok_off[nd.seq] + r;            // token within its sequence
+            const int32_t ob = a.old_blk_off[nd.seq] + t / bo;
+            slot = t - (t / bo) * bo;
+            bool ok = ob >= 0 && ob < a.n_old_desc;
+            BlockDesc od{0, 0, 0, 0};
+            if (ok) {
+                od = a.old_desc[ob];
+                ok = od.seq == nd.seq && slot < od.n;
+            }
+            if (ok)
+                base = (kv ? it.src_v : it.src_k) + static_cast<uint64_t>(od.block) * a.old_block_stride +
+                       static_cast<uint64_t>(j) * a.old_head_step;
+            else
+                *a.flag = 1;
+        }
+        s_src[x] = base;
+        s_slot[x] = slot;
+    }
+    __syncthreads();
+
+    const uint32_t vph = static_cast<uint32_t>(hb / 16);
+    const uint32_t per_tile = static_cast<uint32_t>(bn) * vph;
+    const uint32_t total = static_cast<uint32_t>(nt) * per_tile;
+    const uint32_t lrow = static_cast<uint32_t>(a.lds_row);
+    const uint32_t tile_lds = static_cast<uint32_t>(bn) * lrow;
+    const int32_t m = 16 / eb;                                      // elements per vector
+
+    if (a.old_layout == a.new_layout && bo == bn) {
+        // Same tile layout and block size: a new block holds the same tokens at the same slots as one
+        // old block (blocks start at sequence starts), so each tile is copied vector for vector in
+        // its own order, live slots only, without LDS.
+        for (uint32_t x = tid; x < total; x += kTileThreads) {
+            const uint32_t i = fast_div(x, a.rows_magic, a.rows_shift);
+            const uint32_t v = x - i * per_tile;
+            const int32_t n = s_n[i];
+            const uint64_t src0 = s_src[i * bn];
+            if (src0 == 0) continue;
+            const V4* src = reinterpret_cast<const V4*>(src0 + uint64_t(v) * 16);
+            V4* dst = reinterpret_cast<V4*>(s_dst[i] + uint64_t(v) * 16);
+            if (a.new_layout == kLayoutHND || s_kv[i] == 0) {
+                uint32_t r;
+                if (a.new_layout == kLayoutHND) {
+                    r = fast_div(v, a.vph_magic, a.vph_shift);
+                } else {                                                 // [dim / x][slot][x]
+                    const uint32_t c = fast_div(v, a.bn_magic, a.bn_shift);
+                    r = v - c * bn;
+                }
+                if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+                    __builtin_nontemporal_store(__builtin_nontemporal_load(src), dst);
+            } else {                                                     // [dim][slot]
+                const uint32_t e0 = v * m;
+                const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
+                const uint32_t s0 = e0 - dim * bn;
+                int32_t live = min(m, n - static_cast<int32_t>(s0));
+                for (int k = 0; k < live; ++k)
+                    if (s_src[i * bn + s0 + k] == 0) live = k;
+                if (live <= 0) continue;
+                const V4 val = __builtin_nontemporal_load(src);
+                if (live == m) __builtin_nontemporal_store(val, dst);
+                else store_prefix(val, dst, live * eb, eb);
+            }
+        }
+        return;
+    }
+
+    // phase 1: live rows of every tile from the old pool into LDS, token-major
+    for (uint32_t x = tid; x < total; x += kTileThreads) {
+        const uint32_t i = fast_div(x, a.rows_magic, a.rows_shift);
+        const uint32_t rem = x - i * per_tile;
+        const uint32_t r = fast_div(rem, a.vph_magic, a.vph_shift);
+        const uint32_t c = rem - r * vph;
+        const uint64_t base = s_src[i * bn + r];
+        if (static_cast<int32_t>(r) >= s_n[i] || base == 0) continue;
+        const uint32_t slot = static_cast<uint32_t>(s_slot[i * bn + r]);
+        V4 val;
+        if (a.old_layout == kLayoutNHD) {
+            val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(base + uint64_t(slot) * a.old_row_stride + c * 16));
+        } else if (a.old_layout == kLayoutHND) {
+            val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(base + uint64_t(slot) * hb + c * 16));
+        } else if (s_kv[i] == 0) {                                       // [dim / x][slot][x]
+            val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(base + uint64_t(c) * bo * 16 + slot * 16));
+        } else {                                                         // [dim][slot]: element-wise
+            unsigned char* vb = reinterpret_cast<unsigned char*>(&val);
+            const unsigned char* src = reinterpret_cast<const unsigned char*>(base) + uint64_t(c) * m * bo * eb +
+                                       uint64_t(slot) * eb;
+            for (int k = 0; k < m; ++k) {
+                const unsigned char* e = src + uint64_t(k) * bo * eb;
+                if (eb == 2) *reinterpret_cast<unsigned short*>(vb + 2 * k) = *reinterpret_cast<const unsigned short*>(e);
+                else if (eb == 4) *reinterpret_cast<unsigned int*>(vb + 4 * k) = *reinterpret_cast<const unsigned int*>(e);
+                else vb[k] = *e;
+            }
+        }
+        *reinterpret_cast<V4*>(lds + i * tile_lds + r * lrow + c * 16) = val;
+    }
+    __syncthreads();
+
+    // phase 2: every tile into the new pool in its layout, live slots only
+    for (uint32_t x = tid; x < total; x += kTileThreads) {
+        const uint32_t i = fast_div(x, a.rows_magic, a.rows_shift);
+        const uint32_t v = x - i * per_tile;                            // vector of the tile in its own order
+        const unsigned char* tl = lds + i * tile_lds;
+        const int32_t n = s_n[i];
+        if (a.new_layout == kLayoutNHD) {
+            const uint32_t r = fast_div(v, a.vph_magic, a.vph_shift);
+            const uint32_t c = v - r * vph;
+            if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+                __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + r * lrow + c * 16),
+                                            reinterpret_cast<V4*>(s_dst[i] + uint64_t(r) * a.new_row_stride + c * 16));
+            continue;
+        }
+        V4* dst = reinterpret_cast<V4*>(s_dst[i] + uint64_t(v) * 16);
+        if (a.new_layout == kLayoutHND) {
+            const uint32_t r = fast_div(v, a.vph_magic, a.vph_shift);
+            if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+                __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + r * lrow + (v - r * vph) * 16), dst);
+        } else if (s_kv[i] == 0) {                                       // [dim / x][slot][x]
+            const uint32_t c = fast_div(v, a.bn_magic, a.bn_shift);
+            const uint32_t r = v - c * bn;
+            if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+                __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + r * lrow + c * 16), dst);
+        } else {                                                         // [dim][slot]
+            const uint32_t e0 = v * m;
+            const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
+            const uint32_t s0 = e0 - dim * bn;
+            int32_t live = min(m, n - static_cast<int32_t>(s0));
+            for (int k = 0; k < live; ++k)                              // rows without a source stay untouched
+                if (s_src[i * bn + s0 + k] == 0) live = k;
+            if (live <= 0) continue;
+            const V4 val = gather_dim(tl + s0 * lrow + dim * eb, lrow, eb);
+            if (live == m) __builtin_nontemporal_store(val, dst);
+            else store_prefix(val, dst, live * eb, eb);
+        }
+    }
+}
+
+
+// ---------------------------------------------------------------------------
 // unpack with whole destination rows
 // ---------------------------------------------------------------------------
 //
@@ -1295,6 +1513,88 @@ static remp_status launch_local_vec(const LocalArgs& a, dim3 grid, bool small, h
     return hip_check(hipGetLastError(), "copy_local launch");
 }
 
+// Local copy when either pool is not NHD: head tiles through LDS.  items carry
+// the slice's first-head offsets in each pool's own layout.
+static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector<HostLocal>& items,
+                                      int32_t old_layout, int32_t new_layout, const char* ws, hipStream_t stream) {
+    const remp_kv_shape& sh = p.shape;
+    const WorkspaceLayout L = workspace_layout(p);
+    const int64_t n_desc = p.new_live_blocks;
+    if (items.empty() || n_desc == 0) return REMP_OK;
+    if (n_desc >= (int64_t(1) << 28)) return fail(REMP_E_UNSUPPORTED, "more than 2^28 live blocks in one call");
+    const int32_t eb = sh.elem_bytes;
+    const int64_t hb = static_cast<int64_t>(sh.head_dim) * eb;
+    if (hb % 16 != 0) return fail(REMP_E_UNSUPPORTED, "head tiles need head_dim * elem_bytes % 16 == 0");
+    const int32_t bo = sh.old_block_size, bn = sh.new_block_size;
+    if (bn > kMaxLocalRows) return fail(REMP_E_UNSUPPORTED, "new block size above the local-copy row limit");
+    const int64_t lds_row = hb + 16;
+    const int64_t tile_lds = bn * lds_row;
+    if (tile_lds > kTileLdsBytes) return fail(REMP_E_UNSUPPORTED, "a head tile does not fit the LDS budget");
+    int64_t T = std::max<int64_t>(1, kTileWgBytes / (bn * hb));
+    T = std::min<int64_t>({T, kTileLdsBytes / tile_lds, kMaxLocalRows / bn, kMaxUnitsPerWg});
+    const int64_t orow = p.own_old.heads_per_rank() * hb, nrow = p.own_new.heads_per_rank() * hb;
+
+    LocalTileArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.new_desc = reinterpret_cast<const BlockDesc*>(ws + L.sorted_new);
+    a.old_desc = reinterpret_cast<const BlockDesc*>(ws + L.desc_old);
+    a.tok_off = reinterpret_cast<const int32_t*>(ws + L.scan_new);
+    a.old_blk_off = reinterpret_cast<const int32_t*>(ws + L.scan_old) + (p.num_seqs + 1);
+    a.flag = reinterpret_cast<int32_t*>(const_cast<char*>(ws));
+    a.old_block_stride = orow * bo;
+    a.new_block_stride = nrow * bn;
+    a.n_new_desc = static_cast<int32_t>(n_desc);
+    a.n_old_desc = static_cast<int32_t>(p.old_live_blocks);
+    a.tiles_per_wg = static_cast<int32_t>(T);
+    a.old_block_size = bo;
+    a.new_block_size = bn;
+    a.head_bytes = static_cast<int32_t>(hb);
+    a.elem_bytes = eb;
+    a.old_layout = old_layout;
+    a.new_layout = new_layout;
+    a.old_row_stride = static_cast<int32_t>(orow);
+    a.new_row_stride = static_cast<int32_t>(nrow);
+    a.old_head_step = static_cast<int32_t>(old_layout == kLayoutNHD ? hb : hb * bo);
+    a.new_head_step = static_cast<int32_t>(new_layout == kLayoutNHD ? hb : hb * bn);
+    a.lds_row = static_cast<int32_t>(lds_row);
+    const FastDiv fv = make_fastdiv(static_cast<uint32_t>(hb / 16));
+    const FastDiv fr = make_fastdiv(static_cast<uint32_t>(bn * (hb / 16)));
+    const FastDiv fb = make_fastdiv(static_cast<uint32_t>(bn));
+    a.vph_magic = fv.magic;
+    a.vph_shift = fv.shift;
+    a.rows_magic = fr.magic;
+    a.rows_shift = fr.shift;
+    a.bn_magic = fb.magic;
+    a.bn_shift = fb.shift;
+    if (g_trace_start) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
+    }
+    for (size_t first = 0; first < items.size(); first += kMaxLocalTileItems) {
+        const size_t cnt = std::min<size_t>(kMaxLocalTileItems, items.size() - first);
+        int32_t max_hc = 1;
+        for (size_t i = 0; i < cnt; ++i) {
+            const HostLocal& h = items[first + i];
+            LocalTileItem& c = a.items[i];
+            c.src_k = h.src_k;
+            c.src_v = h.src_v;
+            c.dst_k = h.dst_k;
+            c.dst_v = h.dst_v;
+            c.heads = static_cast<int32_t>(h.row_bytes / hb);
+            max_hc = std::max(max_hc, c.heads);
+        }
+        const int64_t gx = (n_desc * 2 * max_hc + T - 1) / T;
+        if (gx > 0x7FFFFFFF) return fail(REMP_E_UNSUPPORTED, "too many head tiles for one launch");
+        // 32-bit vector indices per workgroup: T tiles of bn rows of hb / 16 vectors
+        hipLaunchKernelGGL(copy_local_tiles, dim3(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt)),
+                           dim3(kTileThreads), static_cast<size_t>(T * tile_lds), stream, a);
+        if (remp_status st = hip_check(hipGetLastError(), "copy_local_tiles launch")) return st;
+    }
+    if (g_trace_stop) {
+        if (remp_status st = hip_check(hipEventRecord(g_trace_stop, stream), "trace stop event")) return st;
+    }
+    return REMP_OK;
+}
+
 static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostLocal>& items, const char* ws,
                                 hipStream_t stream) {
     const remp_kv_shape& sh = p.shape;
@@ -1487,8 +1787,6 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
     if (remp_status st = check_pool(plan, dst, plan->own_new.layers_of_rank(rank), plan->shape.new_block_size,
                                     "destination"))
         return st;
-    if (src->layout != kLayoutNHD || dst->layout != kLayoutNHD)
-        return fail(REMP_E_UNSUPPORTED, "the local copy handles NHD pools only");
     if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     if (src->num_blocks < plan->old_num_blocks)
         return fail(REMP_E_SIZE, "source pool has fewer blocks than the old tables address");
@@ -1520,11 +1818,14 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
             for (uint64_t b : d2)
                 if (ranges_overlap(a, old_layer_bytes, b, new_layer_bytes))
                     return fail(REMP_E_INVALID, "old and new storage of layer " + std::to_string(it.layer) + " overlap");
+        // offset of the slice's first head: a row run in NHD, a whole head tile in the tile layouts
+        const uint64_t ostep = src->layout == kLayoutNHD ? hrow : hrow * sh.old_block_size;
+        const uint64_t nstep = dst->layout == kLayoutNHD ? hrow : hrow * sh.new_block_size;
         HostLocal h;
-        h.src_k = s2[0] + static_cast<uint64_t>(it.head_begin - plan->own_old.first_head(rank)) * hrow;
-        h.src_v = s2[1] + static_cast<uint64_t>(it.head_begin - plan->own_old.first_head(rank)) * hrow;
-        h.dst_k = d2[0] + static_cast<uint64_t>(it.head_begin - plan->own_new.first_head(rank)) * hrow;
-        h.dst_v = d2[1] + static_cast<uint64_t>(it.head_begin - plan->own_new.first_head(rank)) * hrow;
+        h.src_k = s2[0] + static_cast<uint64_t>(it.head_begin - plan->own_old.first_head(rank)) * ostep;
+        h.src_v = s2[1] + static_cast<uint64_t>(it.head_begin - plan->own_old.first_head(rank)) * ostep;
+        h.dst_k = d2[0] + static_cast<uint64_t>(it.head_begin - plan->own_new.first_head(rank)) * nstep;
+        h.dst_v = d2[1] + static_cast<uint64_t>(it.head_begin - plan->own_new.first_head(rank)) * nstep;
         h.row_bytes = static_cast<uint32_t>(it.head_count * hrow);
         items.push_back(h);
     }
@@ -1540,6 +1841,8 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
     if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new, L.bucket_new,
                                          L.sorted_new, stream))
         return st;
+    if (src->layout != kLayoutNHD || dst->layout != kLayoutNHD)
+        return launch_local_tiles(*plan, items, src->layout, dst->layout, ws, stream);
     return launch_local(*plan, items, ws, stream);
 }
 

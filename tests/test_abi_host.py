@@ -408,10 +408,10 @@ def test_layout_validation_errors():
         rk.remp_kv_pack(s4["p"].handle, 0, 0, s4["L"], rk.PoolArg(k4, v4, 64, layout=rk.LAYOUT_HND), s4["dev"],
                         rk.buffers(s4["out0"]), s4["ws"], s4["ws_bytes"], 0, 0)
     assert ei.value.status_name == "REMP_E_UNSUPPORTED"
-    # the local copy is NHD only
+    # the local copy through head tiles has the same 16-byte head-row requirement
     with pytest.raises(rk.RempError) as ei:
-        rk.remp_kv_copy_local(p.handle, 0, 0, L, rk.PoolArg(k, v, 64, layout=rk.LAYOUT_HND), s["dev"], s["dst"],
-                              rk.HostTables.of(s["new_t"]), s["dev"], s["ws"], s["ws_bytes"], 0)
+        rk.remp_kv_copy_local(s4["p"].handle, 0, 0, s4["L"], rk.PoolArg(k4, v4, 64, layout=rk.LAYOUT_HND), s4["dev"],
+                              s4["dst"], rk.HostTables.of(s4["new_t"]), s4["dev"], s4["ws"], s4["ws_bytes"], 0)
     assert ei.value.status_name == "REMP_E_UNSUPPORTED"
 
 

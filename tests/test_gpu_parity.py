@@ -335,19 +335,25 @@ def _upload_layout(arrays, layout, layers_of_rank, num_blocks):
 LAYOUT_CASES = [(0, 1), (1, 0), (0, 2), (2, 0), (2, 2), (1, 2), (2, 1)]
 
 
-@pytest.mark.parametrize("lo,ln", LAYOUT_CASES)
-@pytest.mark.parametrize("shape", ["gqa70b", "mha7b_reblock", "fp8", "replicated"])
-def test_layouts(shape, lo, ln):
-    rk = _rk()
+def _layout_workload(shape):
     base = dict(name="layout", num_layers=4, num_kv_heads=8, head_dim=128, elem_bytes=2, dtype="bf16",
                 old_block_size=16, new_block_size=16, num_seqs=5, length_law=("uniform", 0, 150),
                 pool_law=("slack", 1.3), old_topo=(8, 1), new_topo=(4, 2), role="all", seed=41)
     extra = {"gqa70b": {}, "mha7b_reblock": dict(num_kv_heads=16, old_topo=(4, 1), new_topo=(2, 2),
                                                  new_block_size=32),
              "fp8": dict(elem_bytes=1, dtype="fp8", old_block_size=16, new_block_size=32),
-             "replicated": dict(num_kv_heads=4, old_topo=(8, 1), new_topo=(2, 2))}[shape]
+             "replicated": dict(num_kv_heads=4, old_topo=(8, 1), new_topo=(2, 2)),
+             "shrink": dict(num_kv_heads=4, old_topo=(4, 1), new_topo=(2, 1), old_block_size=32,
+                            new_block_size=16)}[shape]
     base.update(extra)
-    w = synthkv.KVWorkload(**base)
+    return synthkv.KVWorkload(**base)
+
+
+@pytest.mark.parametrize("lo,ln", LAYOUT_CASES)
+@pytest.mark.parametrize("shape", ["gqa70b", "mha7b_reblock", "fp8", "replicated"])
+def test_layouts(shape, lo, ln):
+    rk = _rk()
+    w = _layout_workload(shape)
     inp = synthkv.make_inputs(w)
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables)
@@ -377,6 +383,57 @@ def test_layouts(shape, lo, ln):
         want = oracle.staging_buffer(st[p])
         if want.size:
             assert np.array_equal(staging[p].cpu().numpy(), want), f"staging {p}"
+    nd = synthkv.numpy_dtype_for(w.elem_bytes)
+    for q in range(W_new):
+        for l, (kt, vt) in dst[q][1].items():
+            want = oracle.encode_pool(new_host[q][l], ln)
+            assert np.array_equal(kt.cpu().numpy().view(nd), want[0]), f"new rank {q} layer {l} K"
+            assert np.array_equal(vt.cpu().numpy().view(nd), want[1]), f"new rank {q} layer {l} V"
+    for r in range(W_old):                # sources untouched
+        for l, (kt, vt) in src[r][1].items():
+            want = oracle.encode_pool(old_host[r][l], lo)
+            assert np.array_equal(kt.cpu().numpy().view(nd), want[0])
+            assert np.array_equal(vt.cpu().numpy().view(nd), want[1])
+
+
+@pytest.mark.parametrize("lo,ln", LAYOUT_CASES + [(1, 1)])
+@pytest.mark.parametrize("shape", ["gqa70b", "mha7b_reblock", "fp8", "replicated", "shrink"])
+def test_local_fast_path_layouts(shape, lo, ln):
+    """Local fast path with HND / ROCm pools: pack and unpack skip the local slices, copy_local moves them
+    through head tiles; every byte of every new pool must equal the oracle's, in the new layout."""
+    rk = _rk()
+    w = _layout_workload(shape)
+    inp = synthkv.make_inputs(w)
+    L, H = w.num_layers, w.num_kv_heads
+    old_host = hostpools.source_pools(w, inp.old_tables)
+    new_host = hostpools.sentinel_pools(w, inp.new_tables)
+    log(f"[local layout] {shape} old {lo} new {ln}")
+    plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
+    W_old, W_new = plan.info.old_world, plan.info.new_world
+    dto, dtn = DeviceTables(inp.old_tables), DeviceTables(inp.new_tables)
+    src = {r: _upload_layout(old_host[r], lo, rank_layers(r, w.old_topo, L), inp.old_tables.num_blocks)
+           for r in range(W_old)}
+    dst = {q: _upload_layout(new_host[q], ln, rank_layers(q, w.new_topo, L), inp.new_tables.num_blocks)
+           for q in range(W_new)}
+    pairs = [(p.src, p.dst) for p in plan.pairs if p.src != p.dst]
+    staging = staging_for_pairs(plan, w.seed, pairs)
+    ws = Workspace(plan)
+    fl = rk.REMP_KV_SKIP_LOCAL
+    for r in range(W_old):
+        plan.pack(r, src[r][0], dto.dev, window_args(plan, staging, r, W_new, True, 0, L), ws.buf, ws.bytes,
+                  stream_handle(), flags=fl)
+    torch.cuda.synchronize()
+    assert ws.flag() == 0
+    for q in range(W_new):
+        plan.unpack(q, window_args(plan, staging, q, W_old, False, 0, L), dst[q][0], dtn.host, dtn.dev, ws.buf,
+                    ws.bytes, stream_handle(), flags=fl)
+    torch.cuda.synchronize()
+    assert ws.flag() == 0
+    for r in range(min(W_old, W_new)):
+        plan.copy_local(r, src[r][0], dto.dev, dst[r][0], dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle())
+    torch.cuda.synchronize()
+    assert ws.flag() == 0
+    oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables, inp.new_tables)
     nd = synthkv.numpy_dtype_for(w.elem_bytes)
     for q in range(W_new):
         for l, (kt, vt) in dst[q][1].items():

@@ -52,6 +52,8 @@ def parse():
                     help="decoder layers whose weight shards new rank 0 rebuilds from the host store, for the "
                          "workloads with a model (gqa70b: Llama3-70B, qwen30b: Qwen3-30B-A3B, ds32b: "
                          "DeepSeek-R1-Distill-Qwen-32B; 0: skip the weight-shard measurement)")
+    ap.add_argument("--prewarm-gib", type=float, default=200.0,
+                    help="GiB of device memory written and released before the workload is allocated (0: none)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (for counter scaling), then exit")
     return ap.parse_args()
@@ -199,6 +201,18 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     dev = "cuda:0"
+    if args.prewarm_gib > 0:
+        # First use of device memory that no process has used since the box started is measurably
+        # slower for the scattered unpack writes (MI355X: 5.58-5.66 TB/s in a box's first benchmark
+        # process against 5.76-5.84 TB/s in later ones); a serving engine's KV pool is long resident.
+        # Write and release most of the memory once before allocating the workload.
+        free, _ = torch.cuda.mem_get_info()
+        n = min(int(args.prewarm_gib * (1 << 30)), int(free * 0.9))
+        scratch = torch.empty(n, dtype=torch.uint8, device=dev)
+        scratch.fill_(0)
+        torch.cuda.synchronize()
+        del scratch
+        torch.cuda.empty_cache()
     w = synthkv.WORKLOADS[args.workload]
     if w.role == "all":
         print("bench.py times one rank's share; pick a workload with an (old rank, new rank) role",

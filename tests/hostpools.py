@@ -80,3 +80,19 @@ def sentinel_pools(w: synthkv.KVWorkload, tables, ranks=None, layers=None, tag: 
 
 def copy_pools(pools):
     return {r: {l: a.copy() for l, a in d.items()} for r, d in pools.items()}
+
+
+def element_offsets(layout: int, kv: int, blk, slot, hl, d, H_loc: int, bs: int, D: int, elem_bytes: int):
+    """Element index, inside one layer's K or V storage in `layout`, of element (block, slot, local head, dim).
+
+    NHD [nb][bs][H][D]; HND [nb][H][bs][D]; ROCm split: K [nb][H][D/x][bs][x] (x = elements in 16 bytes),
+    V [nb][H][D][bs].  Arguments broadcast (NumPy int64)."""
+    blk, slot, hl, d = (np.asarray(a, dtype=np.int64) for a in (blk, slot, hl, d))
+    if layout == 0:
+        return ((blk * bs + slot) * H_loc + hl) * D + d
+    if layout == 1:
+        return ((blk * H_loc + hl) * bs + slot) * D + d
+    x = 16 // elem_bytes
+    if kv == 0:
+        return (((blk * H_loc + hl) * (D // x) + d // x) * bs + slot) * x + d % x
+    return ((blk * H_loc + hl) * D + d) * bs + slot

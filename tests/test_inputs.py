@@ -78,3 +78,20 @@ def test_hash_is_murmur3_fmix32():
     got = synthkv.words_at(idx, 1, 2, 3)
     want = np.array([fmix(int(i) ^ key) for i in idx], dtype=np.uint32)
     np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("layout", [0, 1, 2])
+@pytest.mark.parametrize("eb", [1, 2, 4])
+def test_element_offsets_match_the_oracle_encoding(layout, eb):
+    """The test harness's layout formula (used to sample full-size pools) against oracle.encode_pool."""
+    import oracle
+    from hostpools import element_offsets
+    nb, bs, H, D = 3, 16, 2, 32
+    dt = synthkv.numpy_dtype_for(eb)
+    rng = np.random.default_rng(eb * 10 + layout)
+    arr = rng.integers(0, np.iinfo(dt).max, size=(2, nb, bs, H, D), dtype=np.uint64).astype(dt)
+    enc = oracle.encode_pool(arr, layout)
+    b, s, h, d = np.meshgrid(np.arange(nb), np.arange(bs), np.arange(H), np.arange(D), indexing="ij")
+    for kv in range(2):
+        off = element_offsets(layout, kv, b, s, h, d, H, bs, D, eb)
+        assert np.array_equal(np.ascontiguousarray(enc[kv]).reshape(-1)[off], arr[kv])

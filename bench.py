@@ -59,6 +59,17 @@ def parse():
     return ap.parse_args()
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def source_hash() -> str:
     with open(KERNEL_SOURCE, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -414,7 +425,7 @@ def main() -> int:
             n_l = len([l for l in sample if p.layer_begin <= l < p.layer_end])
             moved += 2 * n_l * p.slice_bytes * (2 if (key in pairs_out and key in pairs_in) else 1)
         cpu_value = moved / cpu_s / 1e9
-        cpu = {"value": round(cpu_value, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+        cpu = {"value": round(cpu_value, 3), "unit": "GB/s", "cores": 1, "kind": "oracle", "cpu_model": cpu_model(),
                "seconds": round(cpu_s, 2),
                "sample": f"layers {sample} of the same workload and role: pack slices of old rank {ro} "
                          f"and unpack slices of new rank {qn} in those layers ({moved / 1e9:.2f} GB of "
@@ -456,6 +467,8 @@ def main() -> int:
             "pack_bytes": P_pack,
             "unpack_bytes": P_unpack,
             "traffic_bytes": traffic,
+            "payload_GBps": round((P_pack + P_unpack) / (ms_per_step / 1e3) / 1e9, 1),
+            "metadata_bytes": plan.workspace_bytes,
             "pack_kernel_ms": round(pack_avg, 4),
             "unpack_kernel_ms": round(unpack_avg, 4),
         },

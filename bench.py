@@ -194,7 +194,7 @@ def bench_weights(args, rk, synthkv, torch, qn, new_topo, kv_step, kv_ms, dev, s
 def main() -> int:
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU: this build plays one rank's share of the migration on one MI355X "
+        print(f"bench.py runs on one GPU: it plays one rank's share of the migration on one MI355X "
               f"and has no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
         return 2
     if args.copy_calibration > 0:

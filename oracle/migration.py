@@ -11,7 +11,7 @@ does not run the paper's plan construction (Algorithm 1); for every
 (sequence, layer) it reads each head a new rank needs from the old rank that
 supplies it and writes it into the new shard, in NumPy.
 
-Readings of points the paper leaves open (each one is listed in the design doc):
+Readings of points the paper leaves open:
 
 * ownership: pp_owner(l, PP) = l // (L / PP) (equal contiguous layer ranges,
   L % PP == 0) unless the topology carries an explicit partition (stage p

@@ -10,7 +10,7 @@ worker keeps, the tensor rank decides which slice of each partitioned tensor,
 and replicated tensors are kept whole.  In NumPy, per tensor: slice every part
 the way its split says, then stack the slices along rows.
 
-Readings of points the paper leaves open (each one is listed in the design doc):
+Readings of points the paper leaves open:
 
 * ranks and layer ownership as for the KV cache: rank(pp, tp) = pp * TP + tp,
   stage p holds equal contiguous layer ranges or an explicit partition;
@@ -24,7 +24,12 @@ Readings of points the paper leaves open (each one is listed in the design doc):
   up, embedding and LM head split their output rows, the attention output and
   MLP down projections their input columns, norms are replicated;
 * fused GPU tensors stack their parts' slices along rows in part order
-  (Q | K | V, gate | up).
+  (Q | K | V, gate | up);
+* Q/K/V biases split by heads like their weights; per-head Q/K norm weights
+  and the router of a mixture of experts are replicated; every expert's
+  gate / up rows and down columns are split like a dense MLP's.
+The split of every part is an input (the model inventory says it); the
+oracle applies it by the definition above.
 
 Shapes are elements; every array is [rows][cols] of unsigned integers of the
 element width (values are copied, never interpreted).

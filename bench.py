@@ -214,7 +214,7 @@ def main() -> int:
     dev = "cuda:0"
     if args.prewarm_gib > 0:
         # First use of device memory that no process has used since the machine started is measurably
-        # slower for the scattered unpack writes (MI355X: 5.58-5.66 TB/s in a box's first benchmark
+        # slower for the scattered unpack writes (MI355X: 5.58-5.66 TB/s in a machine's first benchmark
         # process against 5.76-5.84 TB/s in later ones); a serving engine's KV pool is long resident.
         # Write and release most of the memory once before allocating the workload.
         free, _ = torch.cuda.mem_get_info()

@@ -54,6 +54,11 @@ def parse():
                          "DeepSeek-R1-Distill-Qwen-32B; 0: skip the weight-shard measurement)")
     ap.add_argument("--prewarm-gib", type=float, default=200.0,
                     help="GiB of device memory written and released before the workload is allocated (0: none)")
+    ap.add_argument("--seed", type=int, default=None, help="override the workload's seed")
+    ap.add_argument("--sigma", type=float, default=None,
+                    help="override the lognormal sigma of the workload's sequence lengths")
+    ap.add_argument("--stream-windows", default="1,10",
+                    help="layers per window for the layer-streaming measurement, comma separated ('' to skip)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (for counter scaling), then exit")
     return ap.parse_args()
@@ -225,6 +230,13 @@ def main() -> int:
         del scratch
         torch.cuda.empty_cache()
     w = synthkv.WORKLOADS[args.workload]
+    if args.seed is not None:
+        w = w.replace(seed=args.seed)
+    if args.sigma is not None:
+        if w.length_law[0] != "lognormal":
+            print(f"--sigma applies to lognormal length laws; {w.name} uses {w.length_law[0]}", file=sys.stderr)
+            return 2
+        w = w.replace(length_law=("lognormal", w.length_law[1], args.sigma, w.length_law[3]))
     if w.role == "all":
         print("bench.py times one rank's share; pick a workload with an (old rank, new rank) role",
               file=sys.stderr)
@@ -379,6 +391,36 @@ def main() -> int:
         log(f"local fast path: {ms_local:.3f} ms/step ({ms_per_step / ms_local:.2f}x), "
             f"{local['hbm_GBps']} GB/s of HBM traffic")
 
+    # --- layer streaming: the same share as one pack and one unpack call per window of layers ---
+    streaming = []
+    for per in [int(x) for x in args.stream_windows.split(",") if x.strip()]:
+        if per < 1 or per >= L:
+            continue
+        wins = [(a, min(L, a + per)) for a in range(0, L, per)]
+        wargs = [(tio.staging_args(staging, ro, W_new, True, plan, x), tio.staging_args(staging, qn, W_old, False,
+                                                                                       plan, x), x) for x in wins]
+
+        def step_windows():
+            for so, si, (a, b) in wargs:
+                plan.pack(ro, src_arg, dto.dev, so, ws, ws.numel(), stream, a, b)
+                plan.unpack(qn, si, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream, a, b)
+
+        for _ in range(args.warmup):
+            step_windows()
+        torch.cuda.synchronize()
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record()
+        for _ in range(args.steps):
+            step_windows()
+        b1.record()
+        torch.cuda.synchronize()
+        if tio.workspace_flag(ws) != 0:
+            raise RuntimeError("device tables disagree with host tables")
+        ms_w = b0.elapsed_time(b1) / max(args.steps, 1)
+        streaming.append({"layers_per_window": per, "windows": len(wins), "ms_per_step": round(ms_w, 4),
+                          "GBps": round(traffic / (ms_w / 1e3) / 1e9, 1)})
+        log(f"layer streaming, {per} layers per window: {ms_w:.3f} ms/step")
+
     weights = None
     spec = WEIGHT_MODELS.get(w.name)
     if args.weight_layers > 0 and spec is not None:
@@ -474,6 +516,7 @@ def main() -> int:
         },
         "roofline": roofline,
         "local_fast_path": local,
+        "layer_streaming": streaming,
         "weights": weights,
         "cpu_baseline": cpu,
     }

@@ -45,7 +45,10 @@ constexpr bool kMergeRows = true;    // unpack whole destination rows when sever
 // within a row costs more read locality than whole-row writes gain (measured
 // on MI355X: 70B GQA unpack 5.17 vs 5.32 TB/s; 7B MHA, 2 KiB shares, +1.3%).
 constexpr uint32_t kMergeMinSegBytes = 1024;
-constexpr int kMaxItems = 96;         // slices per copy launch (kernel arguments stay < 4 KiB)
+// Slices per copy launch.  Launches of a few slices beat one launch of all of them (A/B on MI355X, 70B
+// GQA share: 96 per launch 5.71, 40: 5.73, 10: 5.79-5.83, 5: 5.80, 2: 5.76, 1: 5.66 TB/s), and the kernel
+// arguments stay small.
+constexpr int kMaxItems = 8;
 constexpr int kMaxUnitsPerWg = 128;   // (block, K or V) units per workgroup
 // Copy launch policies (measured on MI355X).  Small (block, K/V) units, as
 // with GQA head rows of 256 B, run fastest as many small workgroups, each
@@ -393,7 +396,7 @@ __global__ __launch_bounds__(THREADS) void copy_slices(const CopyArgs args) {
 // (new block, K or V); the prologue resolves every row of the unit's live
 // tokens to its old (block, slot) through the old descriptors, so the main
 // loop is a row-gather with one LDS lookup per vector.
-constexpr int kMaxLocalItems = 64;
+constexpr int kMaxLocalItems = 8;     // local slices per launch (few per launch measured faster, as for kMaxItems)
 constexpr int kMaxLocalRows = 1024;   // (unit, row) source addresses per workgroup
 
 struct LocalItem {
@@ -714,7 +717,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) 
 // written as 16-byte vectors of the row; the ROCm V layout, where a token's
 // elements of one head lie block_size elements apart, is read element-wise.
 
-constexpr int kMaxLocalTileItems = 48;
+constexpr int kMaxLocalTileItems = 8;
 
 struct LocalTileItem {
     uint64_t src_k, src_v;   // old storage of the layer at the slice's first head (block 0)
@@ -933,7 +936,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
 // the row into source slices.
 
 constexpr int kMaxMergeSegs = 8;
-constexpr int kMaxMergeGroups = 64;
+constexpr int kMaxMergeGroups = 8;
 
 struct MergeSeg {
     uint32_t row_bytes;   // head_count * head_bytes of the slice

@@ -81,7 +81,8 @@ def source_hash() -> str:
 
 
 def measured_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from committed counter runs, if taken on this kernel source."""
+    """HBM bytes per call of `kernel` ("pack" / "unpack") from committed counter runs, if taken on this
+    kernel source."""
     try:
         with open(COUNTERS) as f:
             c = json.load(f)
@@ -90,7 +91,7 @@ def measured_traffic(kernel: str):
     if c.get("source_hash") != source_hash():
         return None
     k = c.get("kernels", {}).get(kernel)
-    return None if k is None else k.get("hbm_bytes_per_launch")
+    return None if k is None else k.get("hbm_bytes_per_call")
 
 
 def copy_calibration(gib: float) -> None:
@@ -441,8 +442,12 @@ def main() -> int:
         "unit": "GB/s",
         "frac": round(achieved / PEAK_HBM_GBS, 4),
         "traffic": measured_traffic(dom),
-        "algorithmic_bytes_per_launch": dom_bytes,
-        "avg_launch_ms": round(dom_ms, 4),
+        # one call launches the kernel once per 8 slices; bytes and time are per call (HIP events around
+        # all of its launches, gaps included)
+        "algorithmic_bytes_per_call": dom_bytes,
+        "avg_call_ms": round(dom_ms, 4),
+        "launches_per_call": -(-sum(pair_info[p].layer_end - pair_info[p].layer_begin
+                                    for p in (pairs_out if dom == "pack" else pairs_in)) // 8),
     }
 
     # --- CPU baseline: the oracle on a bounded sample of the same workload ----

@@ -30,7 +30,9 @@ if ROOT not in sys.path:
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
 PEAK_PCIE_GBS = 64.0   # PCIe Gen5 x16, one direction (32 GT/s x 16 lanes)
 COUNTERS = os.path.join(ROOT, "profiles", "copy_slices_gqa70b_hbm_counters.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_18741_amd", "csrc", "migrate.hip")
+CSRC = os.path.join(ROOT, "paper_2606_18741_amd", "csrc")
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("device_util.hpp", "kv_copy.hpp", "kv_device.hpp", "kv_expand.hpp",
+                                                  "kv_rows.hpp", "kv_tiles.hpp", "migrate.hip")]
 
 
 def log(msg: str) -> None:
@@ -76,8 +78,12 @@ def cpu_model() -> str:
 
 
 def source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the KV-migration GPU sources (launch code and kernels)."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel: str):

@@ -1,0 +1,81 @@
+// Device data structures and launch constants of the KV-migration kernels.
+// Included by migrate.hip only (one translation unit holds every kernel).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "device_util.hpp"
+#include "plan.hpp"
+
+namespace remp {
+
+// ---------------------------------------------------------------------------
+// device data structures
+// ---------------------------------------------------------------------------
+
+// One live block of one sequence: physical block id, position of its first
+// token on the sequence-major token axis, number of live tokens in it, and
+// the sequence it belongs to.
+struct BlockDesc {
+    int32_t block;
+    int32_t tok;
+    int32_t n;
+    int32_t seq;
+};
+
+constexpr bool kMergeRows = true;    // unpack whole destination rows when several sources fill them
+// ... but only when every source's share of a row is at least this long: with
+// short shares (GQA head rows of 256 B) alternating between staging streams
+// within a row costs more read locality than whole-row writes gain (measured
+// on MI355X: 70B GQA unpack 5.17 vs 5.32 TB/s; 7B MHA, 2 KiB shares, +1.3%).
+constexpr uint32_t kMergeMinSegBytes = 1024;
+// Slices per copy launch.  Launches of a few slices beat one launch of all of them (A/B on MI355X, 70B
+// GQA share: 96 per launch 5.71, 40: 5.73, 10: 5.79-5.83, 5: 5.80, 2: 5.76, 1: 5.66 TB/s), and the kernel
+// arguments stay small.
+constexpr int kMaxItems = 8;
+constexpr int kMaxUnitsPerWg = 128;   // (block, K or V) units per workgroup
+// Copy launch policies (measured on MI355X).  Small (block, K/V) units, as
+// with GQA head rows of 256 B, run fastest as many small workgroups, each
+// moving one unit; large units (MHA rows of several KiB) prefer wider
+// workgroups that move about 64 KiB.
+constexpr int64_t kSmallUnitBytes = 16 * 1024;   // units up to this size use the small policy
+constexpr int kSmallThreads = 128, kSmallUnroll = 4;
+constexpr int kPackSmallThreads = 64, kPackSmallUnroll = 4;   // pack of small units: one wave per unit
+// XCD-contiguous cell order, per launch kind (A/B on MI355X, one process: with it, 7B MHA pack
+// +5%; 70B GQA small-unit pack -1.5% and unpack of block-sorted descriptors -1.6%)
+constexpr bool kPackSmallXcd = false;
+constexpr bool kUnpackSmallXcd = false;
+constexpr bool kPackLargeXcd = true;
+constexpr bool kUnpackLargeXcd = true;
+constexpr int64_t kSmallWgBytes = 4 * 1024;
+constexpr int64_t kLocalSmallWgBytes = 8 * 1024;   // the local copy's per-unit prologue wants 2 units (70B GQA: +14%)
+constexpr int kLargeThreads = 256, kLargeUnroll = 8;
+constexpr int64_t kLargeWgBytes = 64 * 1024;
+constexpr int kScanThreads = 1024;
+
+struct CopyItem {
+    uint64_t paged_k;     // K storage of the layer, offset to the slice's first head
+    uint64_t paged_v;
+    uint64_t stage;       // first byte of the slice in its staging buffer (K part)
+    uint32_t row_bytes;   // head_count * head_dim * elem_bytes
+    uint32_t vpr_magic;   // fast division by vectors per row
+    uint32_t unit_magic;  // fast division by vectors per (block, kv) unit
+    uint16_t vpr_shift;
+    uint16_t unit_shift;
+};
+
+struct CopyArgs {
+    const BlockDesc* desc;
+    int64_t block_stride;     // bytes per block on the paged side
+    int64_t total_tokens;     // T: a slice's V part starts T * row_bytes after its K part
+    int32_t n_desc;
+    int32_t units_per_wg;
+    int32_t row_stride;       // bytes per token row on the paged side (all local heads)
+    int32_t block_size;       // paged-side block size
+    CopyItem items[kMaxItems];
+};
+static_assert(sizeof(CopyArgs) < 4096, "copy kernel arguments must stay below 4 KiB");
+
+}  // namespace remp

@@ -407,26 +407,32 @@ def main() -> int:
         wargs = [(tio.staging_args(staging, ro, W_new, True, plan, x), tio.staging_args(staging, qn, W_old, False,
                                                                                        plan, x), x) for x in wins]
 
-        def step_windows():
-            for so, si, (a, b) in wargs:
-                plan.pack(ro, src_arg, dto.dev, so, ws, ws.numel(), stream, a, b)
-                plan.unpack(qn, si, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream, a, b)
+        def step_windows(reuse):
+            # with reuse, the step's first pack and first unpack expand the tables, the other windows
+            # take the descriptors they left in the workspace
+            for i, (so, si, (a, b)) in enumerate(wargs):
+                fl = rk.REMP_KV_REUSE_DESCRIPTORS if (reuse and i) else 0
+                plan.pack(ro, src_arg, dto.dev, so, ws, ws.numel(), stream, a, b, flags=fl)
+                plan.unpack(qn, si, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream, a, b, flags=fl)
 
-        for _ in range(args.warmup):
-            step_windows()
-        torch.cuda.synchronize()
-        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        b0.record()
-        for _ in range(args.steps):
-            step_windows()
-        b1.record()
-        torch.cuda.synchronize()
-        if tio.workspace_flag(ws) != 0:
-            raise RuntimeError("device tables disagree with host tables")
-        ms_w = b0.elapsed_time(b1) / max(args.steps, 1)
-        streaming.append({"layers_per_window": per, "windows": len(wins), "ms_per_step": round(ms_w, 4),
-                          "GBps": round(traffic / (ms_w / 1e3) / 1e9, 1)})
-        log(f"layer streaming, {per} layers per window: {ms_w:.3f} ms/step")
+        row = {"layers_per_window": per, "windows": len(wins)}
+        for reuse in (False, True):
+            for _ in range(args.warmup):
+                step_windows(reuse)
+            torch.cuda.synchronize()
+            b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            b0.record()
+            for _ in range(args.steps):
+                step_windows(reuse)
+            b1.record()
+            torch.cuda.synchronize()
+            if tio.workspace_flag(ws) != 0:
+                raise RuntimeError(f"workspace flag {tio.workspace_flag(ws)} after layer streaming")
+            ms_w = b0.elapsed_time(b1) / max(args.steps, 1)
+            key = "reuse_descriptors" if reuse else "expand_every_call"
+            row[key] = {"ms_per_step": round(ms_w, 4), "GBps": round(traffic / (ms_w / 1e3) / 1e9, 1)}
+            log(f"layer streaming, {per} layers per window, {key.replace('_', ' ')}: {ms_w:.3f} ms/step")
+        streaming.append(row)
 
     weights = None
     spec = WEIGHT_MODELS.get(w.name)

@@ -174,13 +174,26 @@ typedef struct {
 
 typedef struct remp_kv_plan_s remp_kv_plan_t;
 
-/* Flags of remp_kv_pack and remp_kv_unpack. */
+/* Flags of remp_kv_pack, remp_kv_unpack and remp_kv_copy_local. */
 enum {
     /* Leave out the slices whose peer is the calling rank itself (the same
      * global rank id in the old and the new topology).  Those slices stay on
      * the worker (Section 3.4.3, local copy); move them with
-     * remp_kv_copy_local instead of staging them. */
-    REMP_KV_SKIP_LOCAL = 1u
+     * remp_kv_copy_local instead of staging them.  Pack and unpack only. */
+    REMP_KV_SKIP_LOCAL = 1u,
+    /* Reuse the block descriptors an earlier call left in the workspace
+     * instead of expanding the block tables again: the old ones (pack), the
+     * new ones (unpack), or both (copy_local).  Meant for layer-wise streaming
+     * (Section 3.4.4), where every window of a migration reads the same
+     * tables: without it each call spends a few short kernels on the
+     * expansion.  Every call that expands writes a stamp of the plan and the
+     * tables it expanded into the workspace header; a reusing call's kernels
+     * compare it with the stamp of their own plan and tables and, if it
+     * differs (no earlier expansion, another plan, other new tables, or a
+     * workspace overwritten since), copy nothing and set the workspace flag
+     * to 2.  A reusing call leaves the flag otherwise as it was.  Host-side
+     * validation is the same as without the flag. */
+    REMP_KV_REUSE_DESCRIPTORS = 2u
 };
 
 /* Build the migration plan for T_old -> T_new (Section 3.4.2, Algorithm 1:
@@ -210,10 +223,14 @@ REMP_API remp_status remp_kv_plan_get_pair(const remp_kv_plan_t* plan, int32_t i
 REMP_API remp_status remp_kv_plan_query(const remp_kv_plan_t* plan, int32_t src, int32_t dst,
                                int64_t* staging_bytes, int64_t* layer_offsets);
 
-/* Workspace bytes needed by remp_kv_pack and remp_kv_unpack with this plan.
- * The workspace is device memory, 256-byte aligned, owned by the caller.
- * After the stream work of a call completes, its first 4 bytes hold 0 if the
- * device tables agreed with the host tables and a non-zero flag otherwise. */
+/* Workspace bytes needed by remp_kv_pack, remp_kv_unpack and
+ * remp_kv_copy_local with this plan.  The workspace is device memory, 256-byte
+ * aligned, owned by the caller; calls that share one must be ordered (one
+ * stream).  After the stream work of a call that expands the tables completes,
+ * its first 4 bytes (int32) hold 0 if the device tables agreed with the host
+ * tables and 1 otherwise; 2 means a call with REMP_KV_REUSE_DESCRIPTORS found
+ * no matching descriptors and copied nothing.  Bytes 8-23 hold the stamps of
+ * the descriptors; the rest is scratch space of the kernels. */
 REMP_API remp_status remp_kv_workspace_bytes(const remp_kv_plan_t* plan, int64_t* bytes);
 
 /* Pack (Section 3.4.2 send side, Section 3.4.3): for every slice old_rank sends
@@ -225,7 +242,8 @@ REMP_API remp_status remp_kv_workspace_bytes(const remp_kv_plan_t* plan, int64_t
  * nothing in the window may be {NULL, 0}.  Never writes src (the source
  * topology stays intact until the caller commits, Section 3.7).
  * old_tables: device copy of the tables given to remp_kv_plan.
- * flags: 0 or REMP_KV_SKIP_LOCAL (then staging[old_rank] is not used).
+ * flags: REMP_KV_SKIP_LOCAL (then staging[old_rank] is not used) and/or
+ * REMP_KV_REUSE_DESCRIPTORS (old descriptors), or 0.
  * Everything is validated before anything is enqueued; on error nothing is. */
 REMP_API remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank,
                          int32_t layer_begin, int32_t layer_end,
@@ -244,7 +262,9 @@ REMP_API remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank,
  * (REMP_E_INVALID), enough blocks for the live cache (REMP_E_CAPACITY), and
  * dst->num_blocks >= new_tables->num_blocks (REMP_E_SIZE).
  * new_dev_tables: device copy of new_tables.
- * flags: 0 or REMP_KV_SKIP_LOCAL (then staging[new_rank] is not used). */
+ * flags: REMP_KV_SKIP_LOCAL (then staging[new_rank] is not used) and/or
+ * REMP_KV_REUSE_DESCRIPTORS (new descriptors; the new tables must be the ones
+ * the descriptors were expanded from), or 0. */
 REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank,
                            int32_t layer_begin, int32_t layer_end,
                            const remp_buffer* staging,
@@ -267,13 +287,13 @@ REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank
  * (checked per layer, REMP_E_INVALID).  new_tables are validated as in
  * remp_kv_unpack.  old_tables / new_dev_tables: device copies of the tables.
  * The workspace is the one remp_kv_workspace_bytes sizes; nothing is enqueued
- * on error. */
+ * on error.  flags: 0 or REMP_KV_REUSE_DESCRIPTORS (old and new descriptors). */
 REMP_API remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank,
                                int32_t layer_begin, int32_t layer_end,
                                const remp_kv_pool* src, const remp_dev_tables* old_tables,
                                const remp_kv_pool* dst, const remp_block_tables* new_tables,
                                const remp_dev_tables* new_dev_tables,
-                               void* workspace, int64_t workspace_bytes, hipStream_t stream);
+                               void* workspace, int64_t workspace_bytes, uint32_t flags, hipStream_t stream);
 
 /* Measurement hook: while set (non-NULL), the calling thread's pack, unpack
  * and copy_local calls record `start` immediately before and `stop`

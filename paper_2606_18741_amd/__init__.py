@@ -6,7 +6,7 @@ its ctypes binding.  Importing it loads the library and fails loudly when the
 library has not been built: there is no other execution path.
 """
 from . import _lib
-from ._lib import (EXPORTED, LAYOUT_HND, LAYOUT_NHD, LAYOUT_ROCM_SPLIT, REMP_KV_SKIP_LOCAL, STATUS, Buffer, DevTables, HostTables, Plan, PoolArg,
+from ._lib import (EXPORTED, LAYOUT_HND, LAYOUT_NHD, LAYOUT_ROCM_SPLIT, REMP_KV_REUSE_DESCRIPTORS, REMP_KV_SKIP_LOCAL, STATUS, Buffer, DevTables, HostTables, Plan, PoolArg,
                    RempError, buffers, dev_tables, load, remp_kv_copy_local, remp_kv_pack, remp_kv_plan,
                    remp_kv_plan_destroy, remp_kv_plan_get_info, remp_kv_plan_get_pair, remp_kv_plan_query,
                    remp_kv_set_trace_events, remp_kv_unpack, remp_kv_version, remp_kv_workspace_bytes,
@@ -18,7 +18,7 @@ from ._lib import (EXPORTED, LAYOUT_HND, LAYOUT_NHD, LAYOUT_ROCM_SPLIT, REMP_KV_
 load()
 
 __all__ = [
-    "EXPORTED", "LAYOUT_HND", "LAYOUT_NHD", "LAYOUT_ROCM_SPLIT", "REMP_KV_SKIP_LOCAL", "STATUS", "Buffer", "DevTables", "HostTables", "Plan", "PoolArg",
+    "EXPORTED", "LAYOUT_HND", "LAYOUT_NHD", "LAYOUT_ROCM_SPLIT", "REMP_KV_REUSE_DESCRIPTORS", "REMP_KV_SKIP_LOCAL", "STATUS", "Buffer", "DevTables", "HostTables", "Plan", "PoolArg",
     "RempError", "buffers", "dev_tables", "load", "remp_kv_copy_local", "remp_kv_pack", "remp_kv_plan",
     "remp_kv_plan_destroy", "remp_kv_plan_get_info", "remp_kv_plan_get_pair", "remp_kv_plan_query",
     "remp_kv_set_trace_events", "remp_kv_unpack", "remp_kv_version", "remp_kv_workspace_bytes",

@@ -29,6 +29,7 @@ EXPORTED = (
 )
 
 REMP_KV_SKIP_LOCAL = 1
+REMP_KV_REUSE_DESCRIPTORS = 2
 
 # remp_weights.h
 REMP_W_REPLICATED, REMP_W_SPLIT_ROWS, REMP_W_SPLIT_COLS = 0, 1, 2
@@ -138,7 +139,7 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.remp_kv_unpack.restype = st
     lib.remp_kv_copy_local.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(Pool), POINTER(DevTables),
                                        POINTER(Pool), POINTER(BlockTables), POINTER(DevTables), c_void_p, c_int64,
-                                       c_void_p]
+                                       ctypes.c_uint32, c_void_p]
     lib.remp_kv_copy_local.restype = st
     lib.remp_kv_set_trace_events.argtypes = [c_void_p, c_void_p]
     lib.remp_kv_set_trace_events.restype = None
@@ -317,10 +318,10 @@ def remp_kv_unpack(plan, new_rank: int, layer_begin: int, layer_end: int, stagin
 
 def remp_kv_copy_local(plan, rank: int, layer_begin: int, layer_end: int, src: PoolArg, old_dev_tables: DevTables,
                        dst: PoolArg, new_tables: HostTables, new_dev_tables: DevTables, workspace,
-                       workspace_bytes: int, stream: int) -> None:
+                       workspace_bytes: int, flags: int, stream: int) -> None:
     _check(load().remp_kv_copy_local(plan, rank, layer_begin, layer_end, _ref(src), _ref(old_dev_tables),
                                      _ref(dst), _ref(new_tables), _ref(new_dev_tables), _ptr(workspace),
-                                     int(workspace_bytes), c_void_p(stream)), "remp_kv_copy_local")
+                                     int(workspace_bytes), int(flags), c_void_p(stream)), "remp_kv_copy_local")
 
 
 def remp_kv_set_trace_events(start: Optional[int], stop: Optional[int]) -> None:
@@ -473,6 +474,7 @@ class Plan:
 
     def copy_local(self, rank, src: PoolArg, old_dev_tables: DevTables, dst: PoolArg, new_tables: HostTables,
                    new_dev_tables: DevTables, workspace, workspace_bytes, stream, layer_begin: int = 0,
-                   layer_end: Optional[int] = None) -> None:
+                   layer_end: Optional[int] = None, flags: int = 0) -> None:
         remp_kv_copy_local(self.handle, rank, layer_begin, self.num_layers if layer_end is None else layer_end,
-                           src, old_dev_tables, dst, new_tables, new_dev_tables, workspace, workspace_bytes, stream)
+                           src, old_dev_tables, dst, new_tables, new_dev_tables, workspace, workspace_bytes, flags,
+                           stream)

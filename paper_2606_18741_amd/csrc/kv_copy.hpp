@@ -34,13 +34,16 @@ __device__ __forceinline__ void grid_cell(uint32_t* x, uint32_t* y) {
     }
 }
 
-template <int VEC, bool PACK, int THREADS, int UNROLL, bool XCD>
+// CHECK: the call reuses descriptors, so their stamps are compared (the calls
+// that expand their own descriptors run the variant without the comparison).
+template <int VEC, bool PACK, int THREADS, int UNROLL, bool XCD, bool CHECK>
 __global__ __launch_bounds__(THREADS) void copy_slices(const CopyArgs args) {
     typedef typename VecT<VEC>::type V;
     __shared__ uint64_t s_paged[kMaxUnitsPerWg];
     __shared__ uint64_t s_stage[kMaxUnitsPerWg];
     __shared__ int32_t s_n[kMaxUnitsPerWg];
 
+    const bool stale = CHECK && stamps_differ(args.check);   // acted on after the descriptor prologue
     uint32_t cx, cy;
     grid_cell<XCD>(&cx, &cy);
     const CopyItem& it = args.items[cy];
@@ -59,6 +62,10 @@ __global__ __launch_bounds__(THREADS) void copy_slices(const CopyArgs args) {
         s_n[u] = d.n;
     }
     __syncthreads();
+    if (CHECK && stale) {
+        report_stale(args.check);
+        return;
+    }
 
     const uint32_t vpr = it.row_bytes / VEC;
     const uint32_t unit = static_cast<uint32_t>(args.block_size) * vpr;
@@ -124,6 +131,7 @@ struct LocalArgs {
     int32_t units_per_wg;
     int32_t old_row_stride, new_row_stride;
     int32_t old_block_size, new_block_size;
+    StampCheck check;
     LocalItem items[kMaxLocalItems];
 };
 static_assert(sizeof(LocalArgs) < 4096, "local copy kernel arguments must stay below 4 KiB");
@@ -135,6 +143,7 @@ __global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
     __shared__ int32_t s_n[kMaxUnitsPerWg];
     __shared__ uint64_t s_src[kMaxLocalRows];
 
+    if (stale_descriptors(args.check)) return;
     const LocalItem& it = args.items[blockIdx.y];
     const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
     const int32_t nu = min(args.units_per_wg, 2 * args.n_new_desc - u0);
@@ -166,7 +175,7 @@ __global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
                 a = ((g & 1) ? it.src_v : it.src_k) + static_cast<uint64_t>(od.block) * args.old_block_stride +
                     static_cast<uint64_t>(slot) * args.old_row_stride;
             else
-                *args.flag = 1;
+                *args.flag = kFlagTables;
         }
         s_src[i] = a;
     }

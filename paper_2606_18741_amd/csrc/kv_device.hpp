@@ -25,6 +25,41 @@ struct BlockDesc {
     int32_t seq;
 };
 
+// Values of the workspace status flag (int32 at byte 0 of the workspace).
+constexpr int32_t kFlagTables = 1;   // the device tables disagreed with the host tables
+constexpr int32_t kFlagStale = 2;    // a reusing call found descriptors of other tables
+
+// Check of reused descriptors.  A call that expands its own descriptors passes
+// at[] = NULL; a call that reuses them names the stamps they must carry (one
+// per side it reads: old and new).  On a mismatch every workgroup leaves
+// before it writes anything outside LDS, and the first one sets the flag.
+// Kernels whose prologue only reads the descriptor array itself test the
+// result after that prologue (the stamp load then overlaps the descriptor
+// loads); kernels that follow a descriptor to other arrays test it first.
+struct StampCheck {
+    const uint64_t* at[2];
+    uint64_t want[2];
+    int32_t* flag;
+};
+
+__device__ __forceinline__ bool stamps_differ(const StampCheck& c) {
+    bool differ = false;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        if (c.at[i] && *c.at[i] != c.want[i]) differ = true;
+    return differ;
+}
+
+__device__ __forceinline__ void report_stale(const StampCheck& c) {
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *c.flag = kFlagStale;
+}
+
+__device__ __forceinline__ bool stale_descriptors(const StampCheck& c) {
+    if (!stamps_differ(c)) return false;
+    report_stale(c);
+    return true;
+}
+
 constexpr bool kMergeRows = true;    // unpack whole destination rows when several sources fill them
 // ... but only when every source's share of a row is at least this long: with
 // short shares (GQA head rows of 256 B) alternating between staging streams
@@ -74,6 +109,7 @@ struct CopyArgs {
     int32_t units_per_wg;
     int32_t row_stride;       // bytes per token row on the paged side (all local heads)
     int32_t block_size;       // paged-side block size
+    StampCheck check;
     CopyItem items[kMaxItems];
 };
 static_assert(sizeof(CopyArgs) < 4096, "copy kernel arguments must stay below 4 KiB");

@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kScanThreads) void expand_scan(const int32_t* __res
         tok_off[S] = static_cast<int32_t>(carry[0] < INT32_MAX ? carry[0] : INT32_MAX);
         blk_off[S] = static_cast<int32_t>(carry[1] < INT32_MAX ? carry[1] : INT32_MAX);
     }
-    if (bad) *flag = 1;
+    if (bad) *flag = kFlagTables;
 }
 
 // One thread per live block: locate its sequence by binary search over the
@@ -119,8 +119,10 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
                                                    const int32_t* __restrict__ blk_off, int64_t nnz,
                                                    int64_t num_blocks, int64_t total_tokens, int64_t n_desc,
                                                    BlockDesc* __restrict__ desc, int32_t* __restrict__ flag,
-                                                   int32_t* __restrict__ bucket, uint32_t nb) {
+                                                   int32_t* __restrict__ bucket, uint32_t nb,
+                                                   uint64_t* __restrict__ stamp_at, uint64_t stamp) {
     const int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (b == 0 && stamp_at) *stamp_at = stamp;   // the descriptors are complete once this kernel is
     if (b >= n_desc) return;
     int32_t lo = 0, hi = S;   // last s in [0, S] with blk_off[s] <= b
     while (lo < hi) {
@@ -145,7 +147,7 @@ __global__ __launch_bounds__(256) void expand_emit(const int32_t* __restrict__ l
             if (ok) d = BlockDesc{static_cast<int32_t>(id), static_cast<int32_t>(tok), static_cast<int32_t>(cnt), s};
         }
     }
-    if (!ok) *flag = 1;
+    if (!ok) *flag = kFlagTables;
     desc[b] = d;
     if (bucket) atomicAdd(&bucket[block_bucket(d.block, num_blocks > 0 ? num_blocks : 1, nb)], 1);
 }
@@ -216,8 +218,10 @@ __global__ __launch_bounds__(kScanThreads) void sort_scan(int32_t* __restrict__ 
 
 __global__ __launch_bounds__(256) void sort_scatter(const BlockDesc* __restrict__ desc, int32_t n, int64_t num_blocks,
                                                     uint32_t nb, int32_t* __restrict__ next,
-                                                    BlockDesc* __restrict__ out) {
+                                                    BlockDesc* __restrict__ out, uint64_t* __restrict__ stamp_at,
+                                                    uint64_t stamp) {
     const int32_t i = static_cast<int32_t>(blockIdx.x * 256 + threadIdx.x);
+    if (i == 0 && stamp_at) *stamp_at = stamp;   // the sorted descriptors are complete once this kernel is
     if (i < n) {
         const BlockDesc d = desc[i];
         const int32_t pos = atomicAdd(&next[block_bucket(d.block, num_blocks, nb)], 1);

@@ -45,6 +45,7 @@ struct MergeArgs {
     uint32_t unit_magic, unit_shift;   // vectors per (block, K/V) unit
     uint32_t vph_magic, vph_shift;     // vectors per head
     MergeSeg segs[kMaxMergeSegs];
+    StampCheck check;
     uint64_t paged_k[kMaxMergeGroups];
     uint64_t paged_v[kMaxMergeGroups];
     uint64_t stage[kMaxMergeGroups][kMaxMergeSegs / 2];   // filled for nseg <= kMaxMergeSegs / 2
@@ -59,6 +60,7 @@ __global__ __launch_bounds__(THREADS) void unpack_rows(const MergeArgs args) {
     __shared__ int32_t s_n[kMaxUnitsPerWg];
     __shared__ int32_t s_kv[kMaxUnitsPerWg];
 
+    const bool stale = stamps_differ(args.check);   // acted on after the descriptor prologue
     const int32_t g = blockIdx.y;
     const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
     const int32_t nu = min(args.units_per_wg, 2 * args.n_desc - u0);
@@ -73,6 +75,10 @@ __global__ __launch_bounds__(THREADS) void unpack_rows(const MergeArgs args) {
         s_kv[u] = kv;
     }
     __syncthreads();
+    if (stale) {
+        report_stale(args.check);
+        return;
+    }
 
     const uint32_t vpr = static_cast<uint32_t>(args.row_stride) / VEC;
     const uint32_t vph = static_cast<uint32_t>(args.head_bytes) / VEC;

@@ -43,6 +43,7 @@ struct TileArgs {
     uint32_t vpt_magic, vpt_shift;   // division by vectors per tile
     uint32_t vph_magic, vph_shift;   // division by vectors per head row
     uint32_t bs_magic, bs_shift;     // division by block_size
+    StampCheck check;
     CopyItem items[kMaxItems];       // paged_k/v: the slice's first head tile of the layer's block 0
 };
 static_assert(sizeof(TileArgs) < 4096, "tile kernel arguments must stay below 4 KiB");
@@ -107,6 +108,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) 
     __shared__ int32_t s_n[kMaxUnitsPerWg];
     __shared__ int32_t s_kv[kMaxUnitsPerWg];
 
+    const bool stale = stamps_differ(args.check);   // acted on after the descriptor prologue
     const CopyItem& it = args.items[blockIdx.y];
     const int32_t hc = static_cast<int32_t>(it.row_bytes) / args.head_bytes;   // heads in the slice
     const int64_t ntiles = static_cast<int64_t>(args.n_desc) * 2 * hc;
@@ -132,6 +134,10 @@ __global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) 
         s_kv[i] = kv;
     }
     __syncthreads();
+    if (stale) {
+        report_stale(args.check);
+        return;
+    }
 
     const uint32_t vpt = static_cast<uint32_t>(tile_bytes / 16);     // 16-byte vectors per tile
     const uint32_t vph = static_cast<uint32_t>(hb / 16);             // 16-byte vectors per head row
@@ -255,6 +261,7 @@ struct LocalTileArgs {
     uint32_t vph_magic, vph_shift;                // division by vectors per head row
     uint32_t rows_magic, rows_shift;              // division by new_block_size * vectors per head row
     uint32_t bn_magic, bn_shift;                  // division by the new block size
+    StampCheck check;
     LocalTileItem items[kMaxLocalTileItems];
 };
 static_assert(sizeof(LocalTileArgs) < 4096, "local tile kernel arguments must stay below 4 KiB");
@@ -268,6 +275,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
     __shared__ uint64_t s_src[kMaxLocalRows];    // old tile (block, head) base of each (unit, row), 0: none
     __shared__ int32_t s_slot[kMaxLocalRows];
 
+    if (stale_descriptors(a.check)) return;
     const LocalTileItem& it = a.items[blockIdx.y];
     const int32_t hc = it.heads;
     const int64_t ntiles = static_cast<int64_t>(a.n_new_desc) * 2 * hc;
@@ -311,7 +319,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
                 base = (kv ? it.src_v : it.src_k) + static_cast<uint64_t>(od.block) * a.old_block_stride +
                        static_cast<uint64_t>(j) * a.old_head_step;
             else
-                *a.flag = 1;
+                *a.flag = kFlagTables;
         }
         s_src[x] = base;
         s_slot[x] = slot;

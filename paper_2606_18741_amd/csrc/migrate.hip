@@ -56,16 +56,42 @@ struct HostSlice {
 };
 
 
+// Descriptor stamps.  The old descriptors are a function of the plan alone
+// (its old tables), the new ones of the plan and the new tables given to the
+// call, so a stamp is a 64-bit hash of those (never 0, which no expansion
+// writes).  Combination step after Boost's hash_combine, finished with the
+// SplitMix64 output function (Steele, Lea and Flood, 2014).
+static uint64_t mix64(uint64_t h, uint64_t v) { return h ^ (v + 0x9e3779b97f4a7c15ull + (h << 6) + (h >> 2)); }
+
+static uint64_t finish64(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    z ^= z >> 31;
+    return z ? z : 1;
+}
+
+static uint64_t old_stamp(const remp_kv_plan_t& p) { return finish64(mix64(mix64(0, p.serial), 1)); }
+
+static StampCheck no_check(char* ws) {
+    StampCheck c;
+    c.at[0] = c.at[1] = nullptr;
+    c.want[0] = c.want[1] = 0;
+    c.flag = reinterpret_cast<int32_t*>(ws);
+    return c;
+}
+
 static uint32_t sort_buckets(int64_t n_desc) {
     return static_cast<uint32_t>((std::max<int64_t>(n_desc, 1) + kDescsPerBucket - 1) / kDescsPerBucket);
 }
 
 // Enqueue expansion of `tables` into the workspace areas at scan_off / desc_off.
 // With bucket_off >= 0 the expansion also clears and fills the bucket counters
-// of the descriptor sort (new tables only).
+// of the descriptor sort (new tables only).  A non-NULL stamp_at receives
+// `stamp` in the same launch that writes the descriptors.
 static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables& dt, int32_t bs, int64_t nnz,
                                  int64_t num_blocks, int64_t n_desc, char* ws, int64_t scan_off, int64_t desc_off,
-                                 bool reset_flag, hipStream_t stream, int64_t bucket_off = -1) {
+                                 bool reset_flag, hipStream_t stream, int64_t bucket_off, uint64_t* stamp_at,
+                                 uint64_t stamp) {
     if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
     int32_t* flag = reinterpret_cast<int32_t*>(ws);
     int32_t* tok_off = reinterpret_cast<int32_t*>(ws + scan_off);
@@ -80,16 +106,17 @@ static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables&
         const int64_t blocks = (n_desc + 255) / 256;
         hipLaunchKernelGGL(expand_emit, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, dt.seq_lens,
                            dt.row_offsets, dt.block_ids, p.num_seqs, bs, tok_off, blk_off, nnz, num_blocks,
-                           p.total_tokens, n_desc, desc, flag, bucket, nb);
+                           p.total_tokens, n_desc, desc, flag, bucket, nb, stamp_at, stamp);
         if (remp_status st = hip_check(hipGetLastError(), "expand_emit launch")) return st;
     }
     return REMP_OK;
 }
 
 // Finish the bucket sort of the n_desc new descriptors at desc_off (counted by
-// the expansion into bucket_off) into sorted_off.
+// the expansion into bucket_off) into sorted_off; stamp_at receives `stamp`.
 static remp_status launch_sort_new(int64_t n_desc, int64_t num_blocks, char* ws, int64_t desc_off,
-                                   int64_t bucket_off, int64_t sorted_off, hipStream_t stream) {
+                                   int64_t bucket_off, int64_t sorted_off, uint64_t* stamp_at, uint64_t stamp,
+                                   hipStream_t stream) {
     if (n_desc <= 0) return REMP_OK;
     const uint32_t nb = sort_buckets(n_desc);
     const uint32_t grid = static_cast<uint32_t>((n_desc + 255) / 256);
@@ -99,29 +126,38 @@ static remp_status launch_sort_new(int64_t n_desc, int64_t num_blocks, char* ws,
     const int64_t nblk = num_blocks > 0 ? num_blocks : 1;
     hipLaunchKernelGGL(sort_scan, dim3(1), dim3(kScanThreads), 0, stream, cnt, nb);
     hipLaunchKernelGGL(sort_scatter, dim3(grid), dim3(256), 0, stream, desc, static_cast<int32_t>(n_desc), nblk, nb,
-                       cnt, out);
+                       cnt, out, stamp_at, stamp);
     return hip_check(hipGetLastError(), "descriptor sort launch");
 }
 
 // Launch shapes measured on MI355X (70B GQA and 7B MHA shares): small-unit pack runs one wave per
 // 4 KiB unit in plain grid order; everything else takes the XCD-contiguous cell order.
-template <int VEC, bool PACK>
+template <int VEC, bool PACK, bool CHECK>
 static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small && PACK)
-        hipLaunchKernelGGL((copy_slices<VEC, true, kPackSmallThreads, kPackSmallUnroll, kPackSmallXcd>), grid,
+        hipLaunchKernelGGL((copy_slices<VEC, true, kPackSmallThreads, kPackSmallUnroll, kPackSmallXcd, CHECK>), grid,
                            dim3(kPackSmallThreads), 0, stream, a);
     else if (small)
-        hipLaunchKernelGGL((copy_slices<VEC, false, kSmallThreads, kSmallUnroll, kUnpackSmallXcd>), grid,
+        hipLaunchKernelGGL((copy_slices<VEC, false, kSmallThreads, kSmallUnroll, kUnpackSmallXcd, CHECK>), grid,
                            dim3(kSmallThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL((copy_slices<VEC, PACK, kLargeThreads, kLargeUnroll, PACK ? kPackLargeXcd : kUnpackLargeXcd>),
-                           grid, dim3(kLargeThreads), 0, stream, a);
+        hipLaunchKernelGGL(
+            (copy_slices<VEC, PACK, kLargeThreads, kLargeUnroll, PACK ? kPackLargeXcd : kUnpackLargeXcd, CHECK>), grid,
+            dim3(kLargeThreads), 0, stream, a);
+}
+
+template <int VEC, bool PACK>
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_t stream) {
+    if (a.check.at[0] || a.check.at[1])
+        launch_copy_vec<VEC, PACK, true>(a, grid, small, stream);
+    else
+        launch_copy_vec<VEC, PACK, false>(a, grid, small, stream);
 }
 
 template <bool PACK>
 static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSlice>& slices, int64_t n_desc,
                                int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
-                               int64_t desc_off, hipStream_t stream) {
+                               int64_t desc_off, const StampCheck& check, hipStream_t stream) {
     if (slices.empty() || n_desc == 0) return REMP_OK;
     if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
     // widest vector every address and stride is aligned to
@@ -151,6 +187,7 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     a.units_per_wg = C;
     a.row_stride = row_stride;
     a.block_size = bs;
+    a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
     if (gx * kMaxItems >= (int64_t(1) << 32))
         return fail(REMP_E_UNSUPPORTED, "too many block descriptors for one launch");
@@ -194,7 +231,7 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
 template <bool PACK>
 static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostSlice>& slices, int64_t n_desc,
                                 int32_t bs, int64_t block_stride, int32_t layout, const char* ws, int64_t desc_off,
-                                hipStream_t stream) {
+                                const StampCheck& check, hipStream_t stream) {
     if (slices.empty() || n_desc == 0) return REMP_OK;
     if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
     const int32_t eb = p.shape.elem_bytes;
@@ -234,6 +271,7 @@ static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostS
     a.vph_shift = fvph.shift;
     a.bs_magic = fbs.magic;
     a.bs_shift = fbs.shift;
+    a.check = check;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
     }
@@ -295,7 +333,7 @@ static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t head
 
 static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::vector<const HostSlice*>>& groups,
                                int64_t n_desc, int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
-                               int64_t desc_off, hipStream_t stream) {
+                               int64_t desc_off, const StampCheck& check, hipStream_t stream) {
     if (groups.empty() || n_desc == 0) return REMP_OK;
     const int64_t hb = static_cast<int64_t>(p.shape.head_dim) * p.shape.elem_bytes;
     uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(row_stride) |
@@ -322,6 +360,7 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
     a.row_stride = row_stride;
     a.block_size = bs;
     a.head_bytes = static_cast<int32_t>(hb);
+    a.check = check;
     const auto& first = groups.front();
     a.nseg = static_cast<int32_t>(first.size());
     for (size_t i = 0; i < first.size(); ++i)
@@ -411,7 +450,7 @@ static remp_status check_dev_tables(const remp_kv_plan_t* plan, const remp_dev_t
 // New tables describe the planned sequences, every row is long enough, every
 // live id is in range and used once, and the pool can hold the live cache.
 static remp_status check_new_tables(const remp_kv_plan_t* plan, const remp_block_tables* nt,
-                                    const remp_kv_pool* dst, int64_t* nnz_out) {
+                                    const remp_kv_pool* dst, int64_t* nnz_out, uint64_t* stamp_out) {
     if (!nt) return fail(REMP_E_INVALID, "new tables are NULL");
     const remp_block_tables& t = *nt;
     const remp_kv_shape& sh = plan->shape;
@@ -430,6 +469,10 @@ static remp_status check_new_tables(const remp_kv_plan_t* plan, const remp_block
         if (nnz > 0 && !t.block_ids) return fail(REMP_E_INVALID, "new block_ids is NULL");
     }
     std::vector<uint8_t> used(static_cast<size_t>(t.num_blocks), 0);
+    // the new descriptors depend on the plan, the pool size (bounds and sort buckets), the table
+    // length and the ids the expansion reads
+    uint64_t h = mix64(mix64(mix64(mix64(0, plan->serial), 2), static_cast<uint64_t>(t.num_blocks)),
+                       static_cast<uint64_t>(nnz));
     for (int32_t q = 0; q < t.num_seqs; ++q) {
         if (t.seq_lens[q] != plan->seq_lens[q])
             return fail(REMP_E_INVALID, "new tables give sequence " + std::to_string(q) + " length " +
@@ -439,6 +482,7 @@ static remp_status check_new_tables(const remp_kv_plan_t* plan, const remp_block
         if (b < a) return fail(REMP_E_INVALID, "new row_offsets decrease at sequence " + std::to_string(q));
         const int64_t need = ceil_div(t.seq_lens[q], sh.new_block_size);
         if (b - a < need) return fail(REMP_E_INVALID, "new table row of sequence " + std::to_string(q) + " too short");
+        h = mix64(h, static_cast<uint32_t>(a));
         for (int64_t j = 0; j < need; ++j) {
             const int32_t id = t.block_ids[a + j];
             if (id < 0 || id >= t.num_blocks)
@@ -446,9 +490,11 @@ static remp_status check_new_tables(const remp_kv_plan_t* plan, const remp_block
                                               std::to_string(t.num_blocks) + ")");
             if (used[id]) return fail(REMP_E_INVALID, "new block id " + std::to_string(id) + " used twice");
             used[id] = 1;
+            h = mix64(h, static_cast<uint32_t>(id));
         }
     }
     *nnz_out = nnz;
+    *stamp_out = finish64(h);
     return REMP_OK;
 }
 
@@ -525,7 +571,8 @@ static remp_status launch_local_vec(const LocalArgs& a, dim3 grid, bool small, h
 // Local copy when either pool is not NHD: head tiles through LDS.  items carry
 // the slice's first-head offsets in each pool's own layout.
 static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector<HostLocal>& items,
-                                      int32_t old_layout, int32_t new_layout, const char* ws, hipStream_t stream) {
+                                      int32_t old_layout, int32_t new_layout, const char* ws,
+                                      const StampCheck& check, hipStream_t stream) {
     const remp_kv_shape& sh = p.shape;
     const WorkspaceLayout L = workspace_layout(p);
     const int64_t n_desc = p.new_live_blocks;
@@ -547,7 +594,7 @@ static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector
     std::memset(&a, 0, sizeof(a));
     a.new_desc = reinterpret_cast<const BlockDesc*>(ws + L.sorted_new);
     a.old_desc = reinterpret_cast<const BlockDesc*>(ws + L.desc_old);
-    a.tok_off = reinterpret_cast<const int32_t*>(ws + L.scan_new);
+    a.tok_off = reinterpret_cast<const int32_t*>(ws + L.scan_old);
     a.old_blk_off = reinterpret_cast<const int32_t*>(ws + L.scan_old) + (p.num_seqs + 1);
     a.flag = reinterpret_cast<int32_t*>(const_cast<char*>(ws));
     a.old_block_stride = orow * bo;
@@ -575,6 +622,7 @@ static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector
     a.rows_shift = fr.shift;
     a.bn_magic = fb.magic;
     a.bn_shift = fb.shift;
+    a.check = check;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
     }
@@ -605,7 +653,7 @@ static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector
 }
 
 static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostLocal>& items, const char* ws,
-                                hipStream_t stream) {
+                                const StampCheck& check, hipStream_t stream) {
     const remp_kv_shape& sh = p.shape;
     const WorkspaceLayout L = workspace_layout(p);
     const int64_t n_desc = p.new_live_blocks;
@@ -634,7 +682,7 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     std::memset(&a, 0, sizeof(a));
     a.new_desc = reinterpret_cast<const BlockDesc*>(ws + L.sorted_new);
     a.old_desc = reinterpret_cast<const BlockDesc*>(ws + L.desc_old);
-    a.tok_off = reinterpret_cast<const int32_t*>(ws + L.scan_new);
+    a.tok_off = reinterpret_cast<const int32_t*>(ws + L.scan_old);
     a.old_blk_off = reinterpret_cast<const int32_t*>(ws + L.scan_old) + (p.num_seqs + 1);
     a.flag = reinterpret_cast<int32_t*>(const_cast<char*>(ws));
     a.old_block_stride = orow * bo;
@@ -646,6 +694,7 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     a.new_row_stride = static_cast<int32_t>(nrow);
     a.old_block_size = bo;
     a.new_block_size = bn;
+    a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
@@ -702,7 +751,8 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
                          void* workspace, int64_t workspace_bytes_, uint32_t flags, hipStream_t stream) {
     clear_error();
     if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
-    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL)) return fail(REMP_E_INVALID, "unknown flags");
+    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL | REMP_KV_REUSE_DESCRIPTORS))
+        return fail(REMP_E_INVALID, "unknown flags");
     if (old_rank < 0 || old_rank >= plan->own_old.world())
         return fail(REMP_E_RANGE, "old_rank " + std::to_string(old_rank) + " outside [0, " +
                                       std::to_string(plan->own_old.world()) + ")");
@@ -720,19 +770,28 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
     if (remp_status st = collect_slices(*plan, true, old_rank, layer_begin, layer_end, *src, staging,
                                         (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
         return st;
-    if (slices.empty() || plan->old_live_blocks == 0) return REMP_OK;
+    // an empty window or cache does nothing; otherwise the tables are expanded (and their stamp
+    // written) even when the rank has no slice in the window, so that later calls may reuse them
+    if (layer_begin == layer_end || plan->old_live_blocks == 0) return REMP_OK;
     const remp_kv_shape& sh = plan->shape;
     const int64_t row_stride = static_cast<int64_t>(plan->own_old.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
     const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
-    if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz, plan->old_num_blocks,
-                                       plan->old_live_blocks, ws, L.scan_old, L.desc_old, true, stream))
+    uint64_t* old_at = reinterpret_cast<uint64_t*>(ws + L.stamp_old);
+    StampCheck check = no_check(ws);
+    if (flags & REMP_KV_REUSE_DESCRIPTORS) {
+        check.at[0] = old_at;
+        check.want[0] = old_stamp(*plan);
+    } else if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz,
+                                              plan->old_num_blocks, plan->old_live_blocks, ws, L.scan_old, L.desc_old,
+                                              true, stream, -1, old_at, old_stamp(*plan))) {
         return st;
+    }
     if (src->layout != kLayoutNHD)
         return launch_tiles<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size,
-                                  row_stride * sh.old_block_size, src->layout, ws, L.desc_old, stream);
+                                  row_stride * sh.old_block_size, src->layout, ws, L.desc_old, check, stream);
     return launch_copy<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size, row_stride * sh.old_block_size,
-                             static_cast<int32_t>(row_stride), ws, L.desc_old, stream);
+                             static_cast<int32_t>(row_stride), ws, L.desc_old, check, stream);
 }
 
 remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t layer_begin, int32_t layer_end,
@@ -741,7 +800,8 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
                            uint32_t flags, hipStream_t stream) {
     clear_error();
     if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
-    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL)) return fail(REMP_E_INVALID, "unknown flags");
+    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL | REMP_KV_REUSE_DESCRIPTORS))
+        return fail(REMP_E_INVALID, "unknown flags");
     if (new_rank < 0 || new_rank >= plan->own_new.world())
         return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
                                       std::to_string(plan->own_new.world()) + ")");
@@ -752,41 +812,51 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
     if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
     if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
     int64_t nnz = 0;
-    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz)) return st;
+    uint64_t new_stamp = 0;
+    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz, &new_stamp)) return st;
     if (remp_status st = check_dev_tables(plan, new_dev_tables, nnz, "new")) return st;
 
     std::vector<HostSlice> slices;
     if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging,
                                         (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
         return st;
-    if (slices.empty() || plan->new_live_blocks == 0) return REMP_OK;
+    if (layer_begin == layer_end || plan->new_live_blocks == 0) return REMP_OK;   // as in pack
     const remp_kv_shape& sh = plan->shape;
     const int64_t row_stride = static_cast<int64_t>(plan->own_new.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
     const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
-    if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
-                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream, L.bucket_new))
-        return st;
-    if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new, L.bucket_new,
-                                         L.sorted_new, stream))
-        return st;
+    uint64_t* new_at = reinterpret_cast<uint64_t*>(ws + L.stamp_new);
+    StampCheck check = no_check(ws);
+    if (flags & REMP_KV_REUSE_DESCRIPTORS) {
+        check.at[0] = new_at;
+        check.want[0] = new_stamp;
+    } else {
+        if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
+                                           plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream,
+                                           L.bucket_new, nullptr, 0))
+            return st;
+        if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new,
+                                             L.bucket_new, L.sorted_new, new_at, new_stamp, stream))
+            return st;
+    }
     if (dst->layout != kLayoutNHD)
         return launch_tiles<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size,
-                                   row_stride * sh.new_block_size, dst->layout, ws, L.sorted_new, stream);
+                                   row_stride * sh.new_block_size, dst->layout, ws, L.sorted_new, check, stream);
     std::vector<std::vector<const HostSlice*>> groups;
     if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), groups))
         return launch_rows(*plan, groups, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
-                           static_cast<int32_t>(row_stride), ws, L.sorted_new, stream);
+                           static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
     return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
-                              static_cast<int32_t>(row_stride), ws, L.sorted_new, stream);
+                              static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
 }
 
 remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t layer_begin, int32_t layer_end,
                                const remp_kv_pool* src, const remp_dev_tables* old_tables, const remp_kv_pool* dst,
                                const remp_block_tables* new_tables, const remp_dev_tables* new_dev_tables,
-                               void* workspace, int64_t workspace_bytes_, hipStream_t stream) {
+                               void* workspace, int64_t workspace_bytes_, uint32_t flags, hipStream_t stream) {
     clear_error();
     if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (flags & ~static_cast<uint32_t>(REMP_KV_REUSE_DESCRIPTORS)) return fail(REMP_E_INVALID, "unknown flags");
     if (rank < 0 || rank >= plan->own_old.world() || rank >= plan->own_new.world())
         return fail(REMP_E_RANGE, "rank " + std::to_string(rank) + " is not a rank of both topologies");
     if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
@@ -801,7 +871,8 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
         return fail(REMP_E_SIZE, "source pool has fewer blocks than the old tables address");
     if (remp_status st = check_dev_tables(plan, old_tables, plan->old_nnz, "old")) return st;
     int64_t nnz = 0;
-    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz)) return st;
+    uint64_t new_stamp = 0;
+    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz, &new_stamp)) return st;
     if (remp_status st = check_dev_tables(plan, new_dev_tables, nnz, "new")) return st;
 
     const remp_kv_shape& sh = plan->shape;
@@ -838,21 +909,33 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
         h.row_bytes = static_cast<uint32_t>(it.head_count * hrow);
         items.push_back(h);
     }
-    if (items.empty() || plan->new_live_blocks == 0) return REMP_OK;
+    if (layer_begin == layer_end || plan->new_live_blocks == 0) return REMP_OK;   // as in pack
     const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
-    if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz, plan->old_num_blocks,
-                                       plan->old_live_blocks, ws, L.scan_old, L.desc_old, true, stream))
-        return st;
-    if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
-                                       plan->new_live_blocks, ws, L.scan_new, L.desc_new, false, stream, L.bucket_new))
-        return st;
-    if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new, L.bucket_new,
-                                         L.sorted_new, stream))
-        return st;
+    uint64_t* old_at = reinterpret_cast<uint64_t*>(ws + L.stamp_old);
+    uint64_t* new_at = reinterpret_cast<uint64_t*>(ws + L.stamp_new);
+    StampCheck check = no_check(ws);
+    if (flags & REMP_KV_REUSE_DESCRIPTORS) {
+        check.at[0] = old_at;
+        check.want[0] = old_stamp(*plan);
+        check.at[1] = new_at;
+        check.want[1] = new_stamp;
+    } else {
+        if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz,
+                                           plan->old_num_blocks, plan->old_live_blocks, ws, L.scan_old, L.desc_old,
+                                           true, stream, -1, old_at, old_stamp(*plan)))
+            return st;
+        if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
+                                           plan->new_live_blocks, ws, L.scan_new, L.desc_new, false, stream,
+                                           L.bucket_new, nullptr, 0))
+            return st;
+        if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new,
+                                             L.bucket_new, L.sorted_new, new_at, new_stamp, stream))
+            return st;
+    }
     if (src->layout != kLayoutNHD || dst->layout != kLayoutNHD)
-        return launch_local_tiles(*plan, items, src->layout, dst->layout, ws, stream);
-    return launch_local(*plan, items, ws, stream);
+        return launch_local_tiles(*plan, items, src->layout, dst->layout, ws, check, stream);
+    return launch_local(*plan, items, ws, check, stream);
 }
 
 }  // extern "C"

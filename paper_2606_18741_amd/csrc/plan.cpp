@@ -7,6 +7,7 @@
 // non-empty intersection is one item, seen by the old rank as a send and by
 // the new rank as a receive.  The plan carries no device memory.
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <limits>
 #include <new>
@@ -35,9 +36,12 @@ const Pair* find_pair(const remp_kv_plan_t& p, int32_t src, int32_t dst) {
 
 static int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
 
-// Workspace: [mismatch flag, 256 B][old scan][new scan][old descriptors][new descriptors], 256-aligned.
+// Workspace: [header: flag, descriptor stamps; 256 B][old scan][new scan][old descriptors]
+// [new descriptors][bucket counters][sorted new descriptors], each area 256-aligned.
 WorkspaceLayout workspace_layout(const remp_kv_plan_t& p) {
     WorkspaceLayout w;
+    w.stamp_old = 8;
+    w.stamp_new = 16;
     const int64_t scan = align256(2 * (static_cast<int64_t>(p.num_seqs) + 1) * 4);
     w.scan_old = 256;
     w.scan_new = w.scan_old + scan;
@@ -108,6 +112,8 @@ remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo, c
 
     remp_kv_plan_t* p = new (std::nothrow) remp_kv_plan_t();
     if (!p) return fail(REMP_E_INVALID, "out of host memory");
+    static std::atomic<uint64_t> next_serial{1};
+    p->serial = next_serial.fetch_add(1);
     p->old_topo = *old_topo;
     p->new_topo = *new_topo;
     p->shape = s;

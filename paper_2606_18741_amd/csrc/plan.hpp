@@ -75,6 +75,7 @@ struct remp_kv_plan_s {
     std::vector<remp::Item> items;     // Algorithm 1 order: layer, then new tensor rank, then old tensor rank
     std::vector<remp::Pair> pairs;     // ordered by (src, dst)
     std::vector<int32_t> pair_index;   // [old_world * new_world] -> pair or -1
+    uint64_t serial = 0;               // unique per plan in the process (descriptor stamps)
 };
 
 namespace remp {
@@ -85,13 +86,17 @@ void clear_error();
 
 int64_t ceil_div(int64_t a, int64_t b);
 
-// Byte offsets inside the caller's workspace.  Each scan area holds token and
-// block offsets per sequence ([S+1] int32 each); each descriptor area holds
-// one 16-byte descriptor per live block.  Pack uses the old areas, unpack the
-// new ones, the local copy both.  The new descriptors are also bucket-sorted
-// by physical block (bucket counters, then the sorted copy) so that the
-// unpack side writes the paged pool in ascending address order.
+// Byte offsets inside the caller's workspace.  A 256-byte header holds the
+// status flag (int32 at 0) and the stamps of the old and the new descriptors
+// (uint64 at stamp_old and stamp_new: which plan and tables the descriptors
+// were expanded from, so a later call may reuse them).  Each scan area holds
+// token and block offsets per sequence ([S+1] int32 each); each descriptor
+// area holds one 16-byte descriptor per live block.  Pack uses the old areas,
+// unpack the new ones, the local copy both.  The new descriptors are also
+// bucket-sorted by physical block (bucket counters, then the sorted copy) so
+// that the unpack side writes the paged pool in ascending address order.
 struct WorkspaceLayout {
+    int64_t stamp_old, stamp_new;
     int64_t scan_old, scan_new, desc_old, desc_new, bucket_new, sorted_new, total;
 };
 WorkspaceLayout workspace_layout(const remp_kv_plan_t& p);

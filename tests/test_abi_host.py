@@ -304,7 +304,7 @@ def test_pack_validation_errors():
     ks = list(s["src"]._k)
     ks[0] = ks[0] + 1
     _expect("REMP_E_ALIGN", call, src=rk.PoolArg(ks, list(s["src"]._v), 64))
-    _expect("REMP_E_INVALID", call, flags=2)
+    _expect("REMP_E_INVALID", call, flags=4)
     # with REMP_KV_SKIP_LOCAL the local pair's staging entry may be absent
     local_null = list(s["out0"])
     local_null[0] = None
@@ -361,16 +361,18 @@ def test_copy_local_validation_errors():
     s = _setup()
     p, L, nt = s["p"], s["L"], s["new_t"]
     ok = dict(rank=0, src=s["src"], odev=s["dev"], dst=s["dst"], tables=rk.HostTables.of(nt), ndev=s["dev"],
-              workspace=s["ws"], workspace_bytes=s["ws_bytes"], layer_begin=0, layer_end=L)
+              workspace=s["ws"], workspace_bytes=s["ws_bytes"], layer_begin=0, layer_end=L, flags=0)
 
     def call(**kw):
         a = dict(ok)
         a.update(kw)
         rk.remp_kv_copy_local(p.handle, a["rank"], a["layer_begin"], a["layer_end"], a["src"], a["odev"], a["dst"],
-                              a["tables"], a["ndev"], a["workspace"], a["workspace_bytes"], 0)
+                              a["tables"], a["ndev"], a["workspace"], a["workspace_bytes"], a["flags"], 0)
 
     _expect("REMP_E_RANGE", call, rank=2)
     _expect("REMP_E_RANGE", call, layer_end=L + 1)
+    _expect("REMP_E_INVALID", call, flags=rk.REMP_KV_SKIP_LOCAL)    # pack / unpack only
+    _expect("REMP_E_INVALID", call, flags=4)
     _expect("REMP_E_INVALID", call, src=None)
     _expect("REMP_E_INVALID", call, dst=s["src"])                   # wrong layer count for the new topology
     _expect("REMP_E_ALIGN", call, workspace=s["ws"] + 4)
@@ -411,7 +413,7 @@ def test_layout_validation_errors():
     # the local copy through head tiles has the same 16-byte head-row requirement
     with pytest.raises(rk.RempError) as ei:
         rk.remp_kv_copy_local(s4["p"].handle, 0, 0, s4["L"], rk.PoolArg(k4, v4, 64, layout=rk.LAYOUT_HND), s4["dev"],
-                              s4["dst"], rk.HostTables.of(s4["new_t"]), s4["dev"], s4["ws"], s4["ws_bytes"], 0)
+                              s4["dst"], rk.HostTables.of(s4["new_t"]), s4["dev"], s4["ws"], s4["ws_bytes"], 0, 0)
     assert ei.value.status_name == "REMP_E_UNSUPPORTED"
 
 

@@ -63,6 +63,18 @@ def _reset(dst, new_host, staging):
 @pytest.mark.parametrize("local", [False, True])
 @pytest.mark.parametrize("name,windows", [("tiny", None), ("gqa70b", 8), ("mha7b", 4)])
 def test_graph_replays_match_oracle(name, windows, local):
+    _graph_case(name, windows, local, reuse=False)
+
+
+@pytest.mark.parametrize("local", [False, True])
+@pytest.mark.parametrize("name,windows", [("gqa70b", 8), ("mha7b", 4)])
+def test_graph_replays_with_descriptor_reuse(name, windows, local):
+    """Only the first pack and unpack of the captured step expand the tables; the workspace is cleared
+    between replays, so every replay must write the descriptors and their stamps again."""
+    _graph_case(name, windows, local, reuse=True)
+
+
+def _graph_case(name, windows, local, reuse):
     rk = _rk()
     w = synthkv.WORKLOADS[name]
     if name != "tiny":
@@ -76,21 +88,25 @@ def test_graph_replays_match_oracle(name, windows, local):
     step = L // windows if windows else L
     wins = [(a, min(L, a + step)) for a in range(0, L, step)]
     fl = rk.REMP_KV_SKIP_LOCAL if local else 0
+    ru = rk.REMP_KV_REUSE_DESCRIPTORS if reuse else 0
     args = [(l0, l1, {r: window_args(plan, staging, r, W_new, True, l0, l1) for r in range(W_old)},
              {q: window_args(plan, staging, q, W_old, False, l0, l1) for q in range(W_new)}) for (l0, l1) in wins]
 
     def migrate(stream):
-        for (l0, l1, outs, ins) in args:
+        for i, (l0, l1, outs, ins) in enumerate(args):
             for r in range(W_old):
-                plan.pack(r, src[r].arg, dto.dev, outs[r], ws.buf, ws.bytes, stream, l0, l1, flags=fl)
+                again = ru if (i or r) else 0
+                plan.pack(r, src[r].arg, dto.dev, outs[r], ws.buf, ws.bytes, stream, l0, l1, flags=fl | again)
             for q in range(W_new):
-                plan.unpack(q, ins[q], dst[q].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream, l0, l1, flags=fl)
+                again = ru if (i or q) else 0
+                plan.unpack(q, ins[q], dst[q].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream, l0, l1,
+                            flags=fl | again)
             if local:
                 for r in range(min(W_old, W_new)):
                     plan.copy_local(r, src[r].arg, dto.dev, dst[r].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream,
-                                    l0, l1)
+                                    l0, l1, flags=ru)
 
-    log(f"[graph] capture {w.name} windows={len(wins)} local={local}")
+    log(f"[graph] capture {w.name} windows={len(wins)} local={local} reuse={reuse}")
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):          # warm-up outside the capture
@@ -102,6 +118,8 @@ def test_graph_replays_match_oracle(name, windows, local):
     torch.cuda.synchronize()
     for rep in range(3):
         _reset(dst, new_host, staging)
+        if reuse:
+            ws.buf.zero_()
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()

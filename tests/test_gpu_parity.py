@@ -34,11 +34,13 @@ def _rk():
     return rk
 
 
-def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None, local=False):
+def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None, local=False, reuse=False):
     """Pack every old rank, unpack every new rank, per layer window.  Returns device state.
 
     local: pack and unpack skip the slices a rank keeps, and remp_kv_copy_local
     moves those pool to pool.
+    reuse: only the first pack and the first unpack expand the block tables;
+    every later call (and every local copy) reuses their descriptors.
     """
     rk = _rk()
     L = w.num_layers
@@ -55,33 +57,37 @@ def migrate_all(w, old_tables, new_tables, old_host, new_host, windows=None, loc
     stream = stream_handle()
     flags = []
     fl = rk.REMP_KV_SKIP_LOCAL if local else 0
+    reuse_fl = rk.REMP_KV_REUSE_DESCRIPTORS if reuse else 0
+    first_pack = first_unpack = True
     for (l0, l1) in (windows or [(0, L)]):
         for r in range(W_old):
             plan.pack(r, src[r].arg, dto.dev, window_args(plan, staging, r, W_new, True, l0, l1),
-                      ws.buf, ws.bytes, stream, l0, l1, flags=fl)
+                      ws.buf, ws.bytes, stream, l0, l1, flags=fl | (0 if first_pack else reuse_fl))
+            first_pack = first_pack and l0 == l1
         torch.cuda.synchronize()
         flags.append(ws.flag())
         for q in range(W_new):
             plan.unpack(q, window_args(plan, staging, q, W_old, False, l0, l1), dst[q].arg, dtn.host, dtn.dev,
-                        ws.buf, ws.bytes, stream, l0, l1, flags=fl)
+                        ws.buf, ws.bytes, stream, l0, l1, flags=fl | (0 if first_unpack else reuse_fl))
+            first_unpack = first_unpack and l0 == l1
         torch.cuda.synchronize()
         flags.append(ws.flag())
         if local:
             for r in range(min(W_old, W_new)):
                 plan.copy_local(r, src[r].arg, dto.dev, dst[r].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream,
-                                l0, l1)
+                                l0, l1, flags=reuse_fl)
             torch.cuda.synchronize()
             flags.append(ws.flag())
     return plan, src, dst, staging, flags
 
 
-def check_against_oracle(w, inp, windows=None, log_name="", local=False, identical_replicas=True):
+def check_against_oracle(w, inp, windows=None, log_name="", local=False, identical_replicas=True, reuse=False):
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables, identical_replicas=identical_replicas)
     new_host = hostpools.sentinel_pools(w, inp.new_tables)
-    log(f"[parity] {log_name or w.name}: T={int(inp.lens.sum())} windows={windows} local={local}")
+    log(f"[parity] {log_name or w.name}: T={int(inp.lens.sum())} windows={windows} local={local} reuse={reuse}")
     plan, src, dst, staging, flags = migrate_all(w, inp.old_tables, inp.new_tables, old_host, new_host, windows,
-                                                 local)
+                                                 local, reuse)
     pairs = [(p.src, p.dst) for p in plan.pairs if not (local and p.src == p.dst)]
     st = oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables,
                         inp.new_tables, pairs=pairs)
@@ -445,3 +451,168 @@ def test_local_fast_path_layouts(shape, lo, ln):
             want = oracle.encode_pool(old_host[r][l], lo)
             assert np.array_equal(kt.cpu().numpy().view(nd), want[0])
             assert np.array_equal(vt.cpu().numpy().view(nd), want[1])
+
+
+# ---------------------------------------------------------------------------
+# descriptor reuse across calls (REMP_KV_REUSE_DESCRIPTORS)
+# ---------------------------------------------------------------------------
+
+REUSE_CASES = {
+    # per-layer windows of a layer merge plus head split (staged)
+    "gqa70b_long_layers": (lambda: synthkv.reduced(synthkv.GQA_70B_LONG, num_seqs=3, max_len=200),
+                           [(l, l + 1) for l in range(10)] + [(10, 17), (17, 40), (40, 41), (41, 80)], False),
+    "gqa70b_windows_local": (lambda: synthkv.reduced(synthkv.GQA_70B, num_seqs=5, max_len=300),
+                             [(0, 13), (13, 13), (13, 40), (40, 80)], True),
+    "mha7b_rows_windows": (lambda: synthkv.reduced(synthkv.MHA_7B, num_seqs=4, max_len=200),
+                           [(0, 5), (5, 16), (16, 32)], False),
+    "replicated_local": (lambda: EDGE["replicated_keep_local"], [(0, 3), (3, 8)], True),
+    "reblock_local": (lambda: EDGE["heads_not_nested_reblock"], [(0, 2), (2, 6)], True),
+    "uneven_pp_local": (lambda: EDGE["uneven_pp"], [(0, 1), (1, 4), (4, 5)], True),
+}
+
+
+def _windows_cover(windows, L):
+    cov = sorted((a, b) for a, b in windows if a < b)
+    assert cov[0][0] == 0 and cov[-1][1] == L and all(x[1] == y[0] for x, y in zip(cov, cov[1:])), cov
+
+
+@pytest.mark.parametrize("name", list(REUSE_CASES))
+def test_reuse_descriptors_windows(name):
+    """Windows where only the first pack and unpack expand the tables give the oracle's bytes."""
+    make, windows, local = REUSE_CASES[name]
+    w = make()
+    _windows_cover(windows, w.num_layers)
+    check_against_oracle(w, synthkv.make_inputs(w), windows=windows, local=local, reuse=True, log_name=name)
+
+
+def _reuse_setup(w, inp):
+    rk = _rk()
+    L = w.num_layers
+    plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
+    old_host = hostpools.source_pools(w, inp.old_tables)
+    new_host = hostpools.sentinel_pools(w, inp.new_tables)
+    src = {r: RankPool.from_host(old_host[r], rank_layers(r, w.old_topo, L), inp.old_tables.num_blocks, r)
+           for r in range(plan.info.old_world)}
+    dst = {q: RankPool.from_host(new_host[q], rank_layers(q, w.new_topo, L), inp.new_tables.num_blocks, q)
+           for q in range(plan.info.new_world)}
+    pairs = [(p.src, p.dst) for p in plan.pairs]
+    staging = staging_for_pairs(plan, w.seed, pairs)
+    return plan, old_host, new_host, src, dst, pairs, staging
+
+
+def _unchanged(staging, before, dst, new_host, elem_bytes):
+    for p in before:
+        assert torch.equal(staging[p], before[p]), f"staging {p} written"
+    for q, pool in dst.items():
+        got = pool.host(elem_bytes)
+        for l, a in new_host[q].items():
+            assert np.array_equal(got[l], a), f"new rank {q} layer {l} written"
+
+
+@pytest.mark.parametrize("fill", ["zeros", "random"])
+def test_reuse_without_expansion_copies_nothing(fill):
+    """A reusing call on a workspace that holds no matching descriptors copies nothing and sets flag 2."""
+    rk = _rk()
+    w = synthkv.reduced(synthkv.TINY, num_seqs=4, max_len=120)
+    inp = synthkv.make_inputs(w)
+    L = w.num_layers
+    plan, old_host, new_host, src, dst, pairs, staging = _reuse_setup(w, inp)
+    dto, dtn = DeviceTables(inp.old_tables), DeviceTables(inp.new_tables)
+    before = {p: b.clone() for p, b in staging.items()}
+    ws = Workspace(plan)
+    if fill == "random":
+        g = torch.Generator().manual_seed(5)
+        ws.buf.copy_(torch.randint(0, 256, (ws.bytes,), generator=g, dtype=torch.uint8))
+        ws.set_flag(0)
+    else:
+        ws.buf.zero_()
+    reuse = rk.REMP_KV_REUSE_DESCRIPTORS
+    log(f"[reuse] no expansion, workspace {fill}")
+    plan.pack(0, src[0].arg, dto.dev, window_args(plan, staging, 0, plan.info.new_world, True, 0, L), ws.buf,
+              ws.bytes, stream_handle(), flags=reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 2
+    ws.set_flag(0)
+    plan.unpack(0, window_args(plan, staging, 0, plan.info.old_world, False, 0, L), dst[0].arg, dtn.host, dtn.dev,
+                ws.buf, ws.bytes, stream_handle(), flags=reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 2
+    ws.set_flag(0)
+    plan.copy_local(0, src[0].arg, dto.dev, dst[0].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle(),
+                    flags=reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 2
+    _unchanged(staging, before, dst, new_host, w.elem_bytes)
+
+
+def test_reuse_refuses_other_tables_and_plans():
+    """Descriptors of other new tables, or of another plan, are not reused; the matching ones are."""
+    rk = _rk()
+    w = synthkv.reduced(synthkv.GQA_70B, num_seqs=4, max_len=150)
+    inp = synthkv.make_inputs(w)
+    L, H = w.num_layers, w.num_kv_heads
+    plan, old_host, new_host, src, dst, pairs, staging = _reuse_setup(w, inp)
+    W_old, W_new = plan.info.old_world, plan.info.new_world
+    dto, dtn = DeviceTables(inp.old_tables), DeviceTables(inp.new_tables)
+    # other new tables with the same lengths: the same blocks in another order
+    rows = [inp.new_tables.row(s) for s in range(inp.new_tables.num_seqs)]
+    ids = np.concatenate(rows)[::-1].copy()
+    k, rows_b = 0, []
+    for r in rows:
+        rows_b.append(ids[k:k + len(r)])
+        k += len(r)
+    tables_b = tables_from_rows(inp.new_tables.seq_lens, rows_b, inp.new_tables.num_blocks,
+                                inp.new_tables.block_size)
+    dtb = DeviceTables(tables_b)
+    ws = Workspace(plan)
+    reuse = rk.REMP_KV_REUSE_DESCRIPTORS
+    stream = stream_handle()
+    for r in range(W_old):                 # the first pack expands; the rest reuse
+        plan.pack(r, src[r].arg, dto.dev, window_args(plan, staging, r, W_new, True, 0, L), ws.buf, ws.bytes,
+                  stream, flags=0 if r == 0 else reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 0
+    expect = hostpools.copy_pools(new_host)
+    st = oracle.reshard(old_host, expect, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables, inp.new_tables,
+                        pairs=pairs)
+    for p in pairs:
+        assert np.array_equal(staging[p].cpu().numpy(), oracle.staging_buffer(st[p])), f"staging {p}"
+    # expand tables B, then try to reuse them for tables A: nothing may be written
+    scratch = RankPool.from_host(hostpools.copy_pools(new_host)[0], rank_layers(0, w.new_topo, L),
+                                 inp.new_tables.num_blocks, 0)
+    plan.unpack(0, window_args(plan, staging, 0, W_old, False, 0, L), scratch.arg, dtb.host, dtb.dev, ws.buf,
+                ws.bytes, stream)
+    torch.cuda.synchronize()
+    assert ws.flag() == 0
+    log("[reuse] new tables B expanded; reuse with tables A")
+    plan.unpack(0, window_args(plan, staging, 0, W_old, False, 0, L), dst[0].arg, dtn.host, dtn.dev, ws.buf,
+                ws.bytes, stream, flags=reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 2
+    _unchanged({}, {}, {0: dst[0]}, {0: new_host[0]}, w.elem_bytes)
+    # another plan of the same migration does not match this plan's stamps
+    plan2 = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
+    ws.set_flag(0)
+    plan2.unpack(0, window_args(plan2, staging, 0, W_old, False, 0, L), dst[0].arg, dtb.host, dtb.dev, ws.buf,
+                 ws.bytes, stream, flags=reuse)
+    before = {p: b.clone() for p, b in staging.items()}
+    plan2.pack(1, src[1].arg, dto.dev, window_args(plan2, staging, 1, W_new, True, 0, L), ws.buf, ws.bytes, stream,
+               flags=reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 2
+    _unchanged(staging, before, {0: dst[0]}, {0: new_host[0]}, w.elem_bytes)
+    # expanding tables A again makes them reusable: every new rank, first call included
+    ws.set_flag(0)
+    plan.unpack(0, window_args(plan, staging, 0, W_old, False, 0, 0), dst[0].arg, dtn.host, dtn.dev, ws.buf,
+                ws.bytes, stream, 0, 0)                                       # empty window: no expansion
+    plan.unpack(W_new - 1, window_args(plan, staging, W_new - 1, W_old, False, 0, 1), dst[W_new - 1].arg, dtn.host,
+                dtn.dev, ws.buf, ws.bytes, stream, 0, 1)                     # expands, whatever it holds
+    for q in range(W_new):
+        plan.unpack(q, window_args(plan, staging, q, W_old, False, 0, L), dst[q].arg, dtn.host, dtn.dev, ws.buf,
+                    ws.bytes, stream, flags=reuse)
+    torch.cuda.synchronize()
+    assert ws.flag() == 0
+    for q, pool in dst.items():
+        got = pool.host(w.elem_bytes)
+        for l in expect[q]:
+            assert np.array_equal(got[l], expect[q][l]), f"new rank {q} layer {l}"

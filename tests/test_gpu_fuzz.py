@@ -4,7 +4,9 @@ Shapes, element sizes (1, 2, 4 bytes), head counts with and without
 replication, even and explicit uneven pipeline partitions, block sizes that
 change across the switch, empty and fragmented pools, and layer windows are
 drawn at random (tests/fuzzcases.py); every case runs the staged path over
-random layer windows and the local fast path.
+random layer windows and the local fast path, and (half the seeds each)
+the staged or the local path over random windows with the block
+descriptors expanded once and reused by every later call.
 """
 from __future__ import annotations
 
@@ -27,3 +29,5 @@ def test_random_configuration(seed):
                          log_name=f"fuzz{seed} L{w.num_layers} H{w.num_kv_heads} D{w.head_dim} e{w.elem_bytes} "
                                   f"{w.old_topo}->{w.new_topo} bs {w.old_block_size}->{w.new_block_size}")
     check_against_oracle(w, inp, local=True, log_name=f"fuzz{seed} local")
+    check_against_oracle(w, inp, windows=random_windows(seed + 1000, w.num_layers), local=bool(seed % 2),
+                         reuse=True, log_name=f"fuzz{seed} reuse")

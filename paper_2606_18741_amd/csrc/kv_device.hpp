@@ -66,6 +66,12 @@ constexpr bool kMergeRows = true;    // unpack whole destination rows when sever
 // within a row costs more read locality than whole-row writes gain (measured
 // on MI355X: 70B GQA unpack 5.17 vs 5.32 TB/s; 7B MHA, 2 KiB shares, +1.3%).
 constexpr uint32_t kMergeMinSegBytes = 1024;
+// Pack whole source rows when several destinations split an old rank's heads,
+// under the same rule (A/B on MI355X, pack: 13B TP2 -> TP4, two 2.5 KiB shares,
+// +1.0%; long context, two 256 B shares, +0.7%; DeepSeek-32B TP1 -> TP4, four
+// 512 B shares, -5.5%).
+constexpr bool kPackRows = true;
+constexpr uint32_t kPackRowsMinSegBytes = 1024;
 // Slices per copy launch.  Launches of a few slices beat one launch of all of them (A/B on MI355X, 70B
 // GQA share: 96 per launch 5.71, 40: 5.73, 10: 5.79-5.83, 5: 5.80, 2: 5.76, 1: 5.66 TB/s), and the kernel
 // arguments stay small.

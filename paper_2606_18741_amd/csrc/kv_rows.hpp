@@ -1,4 +1,4 @@
-// Unpack with whole destination rows (unpack_rows).
+// Copies of whole paged rows split among several staging slices (copy_rows).
 // Included by migrate.hip only (one translation unit holds every kernel).
 #pragma once
 
@@ -11,16 +11,18 @@
 namespace remp {
 
 // ---------------------------------------------------------------------------
-// unpack with whole destination rows
+// whole paged rows
 // ---------------------------------------------------------------------------
 //
 // When a new rank receives a layer's heads from several sources, the plain
 // unpack writes each source's head range as its own pass over the new blocks,
-// so every block row is opened once per source.  This variant takes one
-// (layer, new block, K/V) unit per workgroup and writes the unit's rows whole:
-// each 16-byte vector of a row finds the source slice holding its head and
-// reads it from that slice's staging.  All layers of a call share the split of
-// the row into source slices.
+// so every block row is opened once per source; likewise the plain pack reads
+// an old block's rows once per destination when several destinations split
+// its heads.  This variant takes one (layer, paged block, K/V) unit per
+// workgroup and copies the unit's rows whole: each 16-byte vector of a row
+// finds the staging slice holding its head and is read from (unpack) or
+// written to (pack) that slice.  All layers of a call share the split of the
+// row into slices.
 
 constexpr int kMaxMergeSegs = 8;
 constexpr int kMaxMergeGroups = 8;
@@ -37,7 +39,7 @@ struct MergeArgs {
     int64_t total_tokens;
     int32_t n_desc;
     int32_t units_per_wg;
-    int32_t row_stride;       // full destination row
+    int32_t row_stride;       // full paged row (all local heads)
     int32_t block_size;
     int32_t nseg;
     int32_t head_bytes;
@@ -50,10 +52,10 @@ struct MergeArgs {
     uint64_t paged_v[kMaxMergeGroups];
     uint64_t stage[kMaxMergeGroups][kMaxMergeSegs / 2];   // filled for nseg <= kMaxMergeSegs / 2
 };
-static_assert(sizeof(MergeArgs) < 4096, "merged unpack kernel arguments must stay below 4 KiB");
+static_assert(sizeof(MergeArgs) < 4096, "whole-row kernel arguments must stay below 4 KiB");
 
-template <int VEC, int THREADS, int UNROLL>
-__global__ __launch_bounds__(THREADS) void unpack_rows(const MergeArgs args) {
+template <int VEC, bool PACK, int THREADS, int UNROLL>
+__global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
     typedef typename VecT<VEC>::type V;
     __shared__ uint64_t s_paged[kMaxUnitsPerWg];
     __shared__ int32_t s_tok[kMaxUnitsPerWg];
@@ -103,12 +105,14 @@ __global__ __launch_bounds__(THREADS) void unpack_rows(const MergeArgs args) {
                     int32_t sg = 0;
                     while (sg + 1 < args.nseg && h >= args.segs[sg + 1].head0) ++sg;
                     const MergeSeg seg = args.segs[sg];
-                    const uint64_t src = args.stage[g][sg] +
-                                         static_cast<uint64_t>(s_kv[u]) * args.total_tokens * seg.row_bytes +
-                                         static_cast<uint64_t>(s_tok[u] + row) * seg.row_bytes +
-                                         static_cast<uint64_t>(h - seg.head0) * args.head_bytes +
-                                         (c - h * vph) * VEC;
-                    dst[j] = s_paged[u] + static_cast<uint64_t>(row) * args.row_stride + c * VEC;
+                    const uint64_t stage = args.stage[g][sg] +
+                                           static_cast<uint64_t>(s_kv[u]) * args.total_tokens * seg.row_bytes +
+                                           static_cast<uint64_t>(s_tok[u] + row) * seg.row_bytes +
+                                           static_cast<uint64_t>(h - seg.head0) * args.head_bytes +
+                                           (c - h * vph) * VEC;
+                    const uint64_t paged = s_paged[u] + static_cast<uint64_t>(row) * args.row_stride + c * VEC;
+                    const uint64_t src = PACK ? paged : stage;
+                    dst[j] = PACK ? stage : paged;
                     r[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(src));
                     ok[j] = true;
                 }

@@ -292,18 +292,20 @@ static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostS
 }
 
 
-// Unpack with whole destination rows, when every layer of the call receives
-// the same split of its rows into 2..kMaxMergeSegs/2 source slices covering
-// all of the rank's heads.  Returns false (nothing enqueued) if not applicable.
-template <int VEC>
+// Whole paged rows, when every layer of the call splits its rows the same way
+// into 2..kMaxMergeSegs/2 staging slices, each at least min_seg_bytes, that
+// cover all of the rank's heads.  Returns false if not applicable.
+template <int VEC, bool PACK>
 static void launch_rows_vec(const MergeArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small)
-        hipLaunchKernelGGL((unpack_rows<VEC, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0, stream, a);
+        hipLaunchKernelGGL((copy_rows<VEC, PACK, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0, stream,
+                           a);
     else
-        hipLaunchKernelGGL((unpack_rows<VEC, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0, stream, a);
+        hipLaunchKernelGGL((copy_rows<VEC, PACK, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0, stream,
+                           a);
 }
 
-static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t heads_per_rank,
+static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t heads_per_rank, uint32_t min_seg_bytes,
                               std::vector<std::vector<const HostSlice*>>& groups) {
     std::vector<int32_t> layers;
     for (const HostSlice& s : slices)
@@ -317,7 +319,7 @@ static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t head
         if (g.size() < 2 || g.size() > kMaxMergeSegs / 2) return false;
         int32_t next = 0;                                 // slices tile the rank's heads exactly
         for (const HostSlice* s : g) {
-            if (s->head_local != next || s->row_bytes < kMergeMinSegBytes) return false;
+            if (s->head_local != next || s->row_bytes < min_seg_bytes) return false;
             next += s->head_count;
         }
         if (next != heads_per_rank) return false;
@@ -331,6 +333,7 @@ static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t head
     return !groups.empty();
 }
 
+template <bool PACK>
 static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::vector<const HostSlice*>>& groups,
                                int64_t n_desc, int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
                                int64_t desc_off, const StampCheck& check, hipStream_t stream) {
@@ -389,13 +392,13 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
         }
         const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
         switch (vec) {
-            case 16: launch_rows_vec<16>(a, grid, small, stream); break;
-            case 8: launch_rows_vec<8>(a, grid, small, stream); break;
-            case 4: launch_rows_vec<4>(a, grid, small, stream); break;
-            case 2: launch_rows_vec<2>(a, grid, small, stream); break;
-            default: launch_rows_vec<1>(a, grid, small, stream); break;
+            case 16: launch_rows_vec<16, PACK>(a, grid, small, stream); break;
+            case 8: launch_rows_vec<8, PACK>(a, grid, small, stream); break;
+            case 4: launch_rows_vec<4, PACK>(a, grid, small, stream); break;
+            case 2: launch_rows_vec<2, PACK>(a, grid, small, stream); break;
+            default: launch_rows_vec<1, PACK>(a, grid, small, stream); break;
         }
-        if (remp_status st = hip_check(hipGetLastError(), "unpack rows launch")) return st;
+        if (remp_status st = hip_check(hipGetLastError(), PACK ? "pack rows launch" : "unpack rows launch")) return st;
     }
     if (g_trace_stop) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_stop, stream), "trace stop event")) return st;
@@ -790,6 +793,11 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
     if (src->layout != kLayoutNHD)
         return launch_tiles<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size,
                                   row_stride * sh.old_block_size, src->layout, ws, L.desc_old, check, stream);
+    std::vector<std::vector<const HostSlice*>> groups;
+    if (kPackRows && merged_rows_apply(slices, plan->own_old.heads_per_rank(), kPackRowsMinSegBytes, groups))
+        return launch_rows<true>(*plan, groups, plan->old_live_blocks, sh.old_block_size,
+                                 row_stride * sh.old_block_size, static_cast<int32_t>(row_stride), ws, L.desc_old, check,
+                                 stream);
     return launch_copy<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size, row_stride * sh.old_block_size,
                              static_cast<int32_t>(row_stride), ws, L.desc_old, check, stream);
 }
@@ -843,8 +851,8 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
         return launch_tiles<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size,
                                    row_stride * sh.new_block_size, dst->layout, ws, L.sorted_new, check, stream);
     std::vector<std::vector<const HostSlice*>> groups;
-    if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), groups))
-        return launch_rows(*plan, groups, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
+    if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), kMergeMinSegBytes, groups))
+        return launch_rows<false>(*plan, groups, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
                            static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
     return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
                               static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);

@@ -74,5 +74,27 @@ int main(void) {
 
     CHECK(strcmp(remp_status_string(REMP_E_CAPACITY), "REMP_E_CAPACITY") == 0, "status names");
     printf("version %s\n", remp_kv_version());
+
+    /* the headers' constants, for the binding to compare with */
+#define CONST(name) printf("const %s %lld\n", #name, (long long)(name))
+    CONST(REMP_OK);
+    CONST(REMP_E_INVALID);
+    CONST(REMP_E_UNSUPPORTED);
+    CONST(REMP_E_RANGE);
+    CONST(REMP_E_CAPACITY);
+    CONST(REMP_E_ALIGN);
+    CONST(REMP_E_SIZE);
+    CONST(REMP_E_HIP);
+    CONST(REMP_KV_SKIP_LOCAL);
+    CONST(REMP_KV_REUSE_DESCRIPTORS);
+    CONST(REMP_KV_LAYOUT_NHD);
+    CONST(REMP_KV_LAYOUT_HND);
+    CONST(REMP_KV_LAYOUT_ROCM_SPLIT);
+    CONST(REMP_W_REPLICATED);
+    CONST(REMP_W_SPLIT_ROWS);
+    CONST(REMP_W_SPLIT_COLS);
+    CONST(REMP_W_FIRST_STAGE);
+    CONST(REMP_W_LAST_STAGE);
+    CONST(REMP_W_COPY_ENGINE);
     return failures != 0;
 }

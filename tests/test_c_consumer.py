@@ -26,3 +26,13 @@ def test_c99_consumer(tmp_path):
     run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
     assert run.returncode == 0, run.stdout + run.stderr
     assert "FAIL" not in run.stdout and run.stdout.count("ok ") >= 15, run.stdout
+    # every constant of the headers has the same value in the Python binding
+    consts = {ln.split()[1]: int(ln.split()[2]) for ln in run.stdout.splitlines() if ln.startswith("const ")}
+    assert len(consts) == 19, consts
+    status_by_name = {v: k for k, v in rk._lib.STATUS.items()}
+    for name, value in consts.items():
+        if name.startswith("REMP_E_") or name == "REMP_OK":
+            assert status_by_name[name] == value, name
+        else:
+            py = name.replace("REMP_KV_LAYOUT_", "LAYOUT_")
+            assert getattr(rk._lib, py) == value, name

@@ -3,8 +3,10 @@
 The GPU plays old rank r0 (packs everything it sends) and new rank q0 (unpacks
 everything it receives); the staging other old ranks send to q0 is packed by
 the same library from their own generated pools.  Large workloads run in layer
-windows (the paper's layer-wise streaming) to bound memory; the 70B GQA share
-runs as one window, exactly like the benchmark.
+windows (the paper's layer-wise streaming) to bound memory, expanding the
+block tables in the first pack and unpack only and reusing the descriptors in
+every later call; the 70B GQA share runs as one window, exactly like the
+benchmark.
 
 Checked against the oracle:
 * sampled staging rows and sampled new-pool rows (uniform over tokens, plus the
@@ -217,6 +219,10 @@ def test_full_size_sampled(name):
     mask_dev = torch.from_numpy(_live_mask(inp.new_tables)).cuda()
     rng = np.random.default_rng(2024)
     checked = 0
+    # windowed runs stream as a serving engine would: only the first pack and the first unpack expand
+    # the block tables, every later call reuses their descriptors
+    reuse = rk.REMP_KV_REUSE_DESCRIPTORS
+    old_expanded = new_expanded = False
     for (l0, l1) in windows:
         log(f"[fullsize] {name} window [{l0}, {l1}) T={plan.info.total_tokens}")
         win = range(l0, l1)
@@ -232,16 +238,21 @@ def test_full_size_sampled(name):
                                       window=(l0, l1))
             bufs = dict(extra)
             bufs[(r, q)] = staging[(r, q)]
-            plan.pack(r, fp.arg, dto.dev, tio.staging_args(bufs, r, W_new, True), ws, ws.numel(), stream, l0, l1)
+            plan.pack(r, fp.arg, dto.dev, tio.staging_args(bufs, r, W_new, True), ws, ws.numel(), stream, l0, l1,
+                      flags=reuse if old_expanded else 0)
+            old_expanded = True
             torch.cuda.synchronize()
             assert tio.workspace_flag(ws) == 0
             del fp, extra, bufs
         plan.pack(ro, src.arg, dto.dev, tio.staging_args({k: staging[k] for k in pairs_out if k in staging},
-                                                         ro, W_new, True), ws, ws.numel(), stream, l0, l1)
+                                                         ro, W_new, True), ws, ws.numel(), stream, l0, l1,
+                  flags=reuse if old_expanded else 0)
+        old_expanded = True
         torch.cuda.synchronize()
         assert tio.workspace_flag(ws) == 0
         plan.unpack(qn, tio.staging_args({k: staging[k] for k in pairs_in if k in staging}, qn, W_old, False),
-                    dst.arg, dtn.host, dtn.dev, ws, ws.numel(), stream, l0, l1)
+                    dst.arg, dtn.host, dtn.dev, ws, ws.numel(), stream, l0, l1, flags=reuse if new_expanded else 0)
+        new_expanded = True
         torch.cuda.synchronize()
         assert tio.workspace_flag(ws) == 0
         for pair in sorted(set(pairs_out) | set(pairs_in)):

@@ -17,6 +17,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import statistics
@@ -78,11 +79,15 @@ def cpu_model() -> str:
 
 
 def source_hash() -> str:
-    """Hash of the KV-migration GPU sources (launch code and kernels)."""
+    """Hash of the KV-migration GPU sources (launch code and kernels), comments and white space left
+    out, so that only a change of the code itself invalidates counters taken on it."""
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:
-        with open(path, "rb") as f:
-            h.update(f.read())
+        with open(path) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -91,7 +91,11 @@ constexpr bool kUnpackSmallXcd = false;
 constexpr bool kPackLargeXcd = true;
 constexpr bool kUnpackLargeXcd = true;
 constexpr int64_t kSmallWgBytes = 4 * 1024;
-constexpr int64_t kLocalSmallWgBytes = 8 * 1024;   // the local copy's per-unit prologue wants 2 units (70B GQA: +14%)
+// The local copy's per-unit prologue (three dependent descriptor reads) wants several units per
+// workgroup: 16 KiB against 8 KiB, copy_local alone on MI355X (one process, memory prewarmed):
+// 70B GQA -4.7% time, long context -5.8%, Qwen3-30B-A3B -5.6% (DeepSeek-32B -3.6% without the
+// prewarm); 256 threads or 32 KiB were slower (8 KiB against 4 KiB had been +14%).
+constexpr int64_t kLocalSmallWgBytes = 16 * 1024;
 constexpr int kLargeThreads = 256, kLargeUnroll = 8;
 constexpr int64_t kLargeWgBytes = 64 * 1024;
 constexpr int kScanThreads = 1024;

@@ -15,25 +15,6 @@ namespace remp {
 // ---------------------------------------------------------------------------
 
 
-// Workgroup (x, y) of a grid -> the grid cell it works on.  With XCD, the
-// cells are renumbered so that each of the 8 XCDs (the dispatcher deals
-// workgroups to them round-robin in linear order) takes one contiguous range
-// of cells: consecutive chunks of a slice then share an XCD's L2 and stream
-// through neighbouring addresses.  A bijection of the grid onto itself.
-template <bool XCD>
-__device__ __forceinline__ void grid_cell(uint32_t* x, uint32_t* y) {
-    *x = blockIdx.x;
-    *y = blockIdx.y;
-    if (XCD) {
-        const uint32_t total = gridDim.x * gridDim.y;
-        const uint32_t lin = blockIdx.y * gridDim.x + blockIdx.x;
-        const uint32_t q = total / 8, r = total % 8, k = lin % 8;
-        const uint32_t cell = k * q + min(k, r) + lin / 8;
-        *x = cell % gridDim.x;
-        *y = cell / gridDim.x;
-    }
-}
-
 // CHECK: the call reuses descriptors, so their stamps are compared (the calls
 // that expand their own descriptors run the variant without the comparison).
 template <int VEC, bool PACK, int THREADS, int UNROLL, bool XCD, bool CHECK>

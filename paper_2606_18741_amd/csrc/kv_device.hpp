@@ -72,6 +72,10 @@ constexpr uint32_t kMergeMinSegBytes = 1024;
 // 512 B shares, -5.5%).
 constexpr bool kPackRows = true;
 constexpr uint32_t kPackRowsMinSegBytes = 1024;
+// XCD-contiguous cell order for the whole-row kernel, per direction (A/B on
+// MI355X: 13B pack +1.4%, 7B unpack -0.4%).
+constexpr bool kPackRowsXcd = true;
+constexpr bool kUnpackRowsXcd = false;
 // Slices per copy launch.  Launches of a few slices beat one launch of all of them (A/B on MI355X, 70B
 // GQA share: 96 per launch 5.71, 40: 5.73, 10: 5.79-5.83, 5: 5.80, 2: 5.76, 1: 5.66 TB/s), and the kernel
 // arguments stay small.
@@ -99,6 +103,25 @@ constexpr int64_t kLocalSmallWgBytes = 16 * 1024;
 constexpr int kLargeThreads = 256, kLargeUnroll = 8;
 constexpr int64_t kLargeWgBytes = 64 * 1024;
 constexpr int kScanThreads = 1024;
+
+// Workgroup (x, y) of a grid -> the grid cell it works on.  With XCD, the
+// cells are renumbered so that each of the 8 XCDs (the dispatcher deals
+// workgroups to them round-robin in linear order) takes one contiguous range
+// of cells: consecutive chunks of a slice then share an XCD's L2 and stream
+// through neighbouring addresses.  A bijection of the grid onto itself.
+template <bool XCD>
+__device__ __forceinline__ void grid_cell(uint32_t* x, uint32_t* y) {
+    *x = blockIdx.x;
+    *y = blockIdx.y;
+    if (XCD) {
+        const uint32_t total = gridDim.x * gridDim.y;
+        const uint32_t lin = blockIdx.y * gridDim.x + blockIdx.x;
+        const uint32_t q = total / 8, r = total % 8, k = lin % 8;
+        const uint32_t cell = k * q + min(k, r) + lin / 8;
+        *x = cell % gridDim.x;
+        *y = cell / gridDim.x;
+    }
+}
 
 struct CopyItem {
     uint64_t paged_k;     // K storage of the layer, offset to the slice's first head

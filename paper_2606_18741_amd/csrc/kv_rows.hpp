@@ -63,8 +63,10 @@ __global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
     __shared__ int32_t s_kv[kMaxUnitsPerWg];
 
     const bool stale = stamps_differ(args.check);   // acted on after the descriptor prologue
-    const int32_t g = blockIdx.y;
-    const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
+    uint32_t cx, cy;
+    grid_cell<PACK ? kPackRowsXcd : kUnpackRowsXcd>(&cx, &cy);
+    const int32_t g = static_cast<int32_t>(cy);
+    const int32_t u0 = static_cast<int32_t>(cx) * args.units_per_wg;
     const int32_t nu = min(args.units_per_wg, 2 * args.n_desc - u0);
     const int tid = threadIdx.x;
     for (int u = tid; u < nu; u += THREADS) {

@@ -91,9 +91,9 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per call of `kernel` ("pack" / "unpack") from committed counter runs, if taken on this
-    kernel source."""
+def profiled_call(kernel: str):
+    """The committed counter record of the `kernel` call ("pack" / "unpack"), if it was taken on this
+    kernel source: HBM bytes per call, the kernel it launches and its launches per call; else None."""
     try:
         with open(COUNTERS) as f:
             c = json.load(f)
@@ -101,8 +101,7 @@ def measured_traffic(kernel: str):
         return None
     if c.get("source_hash") != source_hash():
         return None
-    k = c.get("kernels", {}).get(kernel)
-    return None if k is None else k.get("hbm_bytes_per_call")
+    return c.get("kernels", {}).get(kernel)
 
 
 def copy_calibration(gib: float) -> None:
@@ -451,20 +450,21 @@ def main() -> int:
     else:
         dom, dom_ms, dom_bytes = "unpack", unpack_avg, 2 * P_unpack
     achieved = dom_bytes / (dom_ms / 1e3) / 1e9
+    prof = profiled_call(dom)
+    kname = prof["kernel"].replace("void remp::", "").split("<")[0] if prof else "copy kernel"
     roofline = {
         "bound": "hbm",
-        "kernel": f"copy_slices ({dom})",
+        "kernel": f"{kname} ({dom})",
         "achieved": round(achieved, 1),
         "peak": PEAK_HBM_GBS,
         "unit": "GB/s",
         "frac": round(achieved / PEAK_HBM_GBS, 4),
-        "traffic": measured_traffic(dom),
-        # one call launches the kernel once per 8 slices; bytes and time are per call (HIP events around
-        # all of its launches, gaps included)
+        "traffic": prof["hbm_bytes_per_call"] if prof else None,
+        # a call launches its kernel once per 8 slices (or 8 layers for whole rows); bytes and time are
+        # per call (HIP events around all of its launches, gaps included)
         "algorithmic_bytes_per_call": dom_bytes,
         "avg_call_ms": round(dom_ms, 4),
-        "launches_per_call": -(-sum(pair_info[p].layer_end - pair_info[p].layer_begin
-                                    for p in (pairs_out if dom == "pack" else pairs_in)) // 8),
+        "launches_per_call": prof["launches_per_call"] if prof else None,
     }
 
     # --- CPU baseline: the oracle on a bounded sample of the same workload ----

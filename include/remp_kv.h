@@ -203,7 +203,9 @@ enum {
  * Copies what it needs from old_tables; the caller may free them afterwards.
  * Validates shape (positive sizes, elem_bytes in {1,2,4}), divisibility
  * (REMP_E_UNSUPPORTED), table structure (REMP_E_INVALID) and old block ids in
- * [0, old_tables->num_blocks) (REMP_E_RANGE).  On failure *out is NULL. */
+ * [0, old_tables->num_blocks) (REMP_E_RANGE); at most 2^31 - 1 live tokens and
+ * fewer than 2^28 live blocks in either block size (REMP_E_UNSUPPORTED).  On
+ * failure *out is NULL. */
 REMP_API remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo,
                          const remp_kv_shape* shape, const remp_block_tables* old_tables,
                          remp_kv_plan_t** out);

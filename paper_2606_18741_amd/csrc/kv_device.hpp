@@ -60,22 +60,22 @@ __device__ __forceinline__ bool stale_descriptors(const StampCheck& c) {
     return true;
 }
 
-constexpr bool kMergeRows = true;    // unpack whole destination rows when several sources fill them
-// ... but only when every source's share of a row is at least this long: with
-// short shares (GQA head rows of 256 B) alternating between staging streams
-// within a row costs more read locality than whole-row writes gain (measured
-// on MI355X: 70B GQA unpack 5.17 vs 5.32 TB/s; 7B MHA, 2 KiB shares, +1.3%).
-constexpr uint32_t kMergeMinSegBytes = 1024;
-// Pack whole source rows when several destinations split an old rank's heads,
-// under the same rule (A/B on MI355X, pack: 13B TP2 -> TP4, two 2.5 KiB shares,
-// +1.0%; long context, two 256 B shares, +0.7%; DeepSeek-32B TP1 -> TP4, four
-// 512 B shares, -5.5%).
+// Whole paged rows (copy_rows) when several staging slices split every row into
+// equal shares: unpack when several sources fill a new rank's rows (shares of at
+// least 256 B), pack when several destinations split an old rank's rows into
+// 256 B shares.  A/B on MI355X against per-slice copies (one process, memory
+// prewarmed, three repetitions): unpack 70B GQA (two 256 B shares) -1.6% time,
+// 7B (two 2 KiB) -2.8%; pack long context (two 256 B) -4%, but 13B (two 2.5 KiB)
+// +1% and DeepSeek-32B (four 512 B) +4%, in either order inside the unit and
+// with or without the XCD cell order: whole rows pay on the pack side only where
+// the per-slice pack would read 256 B fragments of each row.  Inside a unit each
+// share's rows are copied in turn (segment-major); cells in plain order.
+constexpr bool kMergeRows = true;
 constexpr bool kPackRows = true;
-constexpr uint32_t kPackRowsMinSegBytes = 1024;
-// XCD-contiguous cell order for the whole-row kernel, per direction (A/B on
-// MI355X: 13B pack +1.4%, 7B unpack -0.4%).
-constexpr bool kPackRowsXcd = true;
-constexpr bool kUnpackRowsXcd = false;
+constexpr uint32_t kUnpackRowsMinShareBytes = 256;
+constexpr uint32_t kPackRowsMinShareBytes = 256;
+constexpr uint32_t kPackRowsMaxShareBytes = 256;
+constexpr uint32_t kUnpackRowsMaxShareBytes = 0xFFFFFFFFu;
 // Slices per copy launch.  Launches of a few slices beat one launch of all of them (A/B on MI355X, 70B
 // GQA share: 96 per launch 5.71, 40: 5.73, 10: 5.79-5.83, 5: 5.80, 2: 5.76, 1: 5.66 TB/s), and the kernel
 // arguments stay small.

@@ -19,19 +19,15 @@ namespace remp {
 // so every block row is opened once per source; likewise the plain pack reads
 // an old block's rows once per destination when several destinations split
 // its heads.  This variant takes one (layer, paged block, K/V) unit per
-// workgroup and copies the unit's rows whole: each 16-byte vector of a row
-// finds the staging slice holding its head and is read from (unpack) or
-// written to (pack) that slice.  All layers of a call share the split of the
-// row into slices.
+// workgroup and copies the whole unit: the row is split into nseg equal
+// shares (one per staging slice, consecutive heads), and the workgroup copies
+// share 0 of all the unit's rows, then share 1, and so on, so every slice's
+// part of the unit is one contiguous staging range read (unpack) or written
+// (pack) in order, while the paged block is covered whole by one workgroup.
+// All layers of a call share the split of the row into slices.
 
-constexpr int kMaxMergeSegs = 8;
-constexpr int kMaxMergeGroups = 8;
-
-struct MergeSeg {
-    uint32_t row_bytes;   // head_count * head_bytes of the slice
-    uint16_t head0;       // first local head
-    uint16_t head_count;
-};
+constexpr int kMaxMergeSegs = 4;     // slices per row
+constexpr int kMaxMergeGroups = 8;   // layers per launch
 
 struct MergeArgs {
     const BlockDesc* desc;
@@ -41,16 +37,15 @@ struct MergeArgs {
     int32_t units_per_wg;
     int32_t row_stride;       // full paged row (all local heads)
     int32_t block_size;
-    int32_t nseg;
-    int32_t head_bytes;
-    uint32_t vpr_magic, vpr_shift;     // vectors per full row
-    uint32_t unit_magic, unit_shift;   // vectors per (block, K/V) unit
-    uint32_t vph_magic, vph_shift;     // vectors per head
-    MergeSeg segs[kMaxMergeSegs];
+    int32_t nseg;             // shares per row
+    uint32_t seg_bytes;       // bytes of one share of a row (= row_stride / nseg)
+    uint32_t unit_magic, unit_shift;   // division by vectors per (block, K/V) unit
+    uint32_t seg_magic, seg_shift;     // division by vectors per share of a unit (block_size * share vectors)
+    uint32_t vps_magic, vps_shift;     // division by vectors per share of a row
     StampCheck check;
     uint64_t paged_k[kMaxMergeGroups];
     uint64_t paged_v[kMaxMergeGroups];
-    uint64_t stage[kMaxMergeGroups][kMaxMergeSegs / 2];   // filled for nseg <= kMaxMergeSegs / 2
+    uint64_t stage[kMaxMergeGroups][kMaxMergeSegs];
 };
 static_assert(sizeof(MergeArgs) < 4096, "whole-row kernel arguments must stay below 4 KiB");
 
@@ -63,10 +58,8 @@ __global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
     __shared__ int32_t s_kv[kMaxUnitsPerWg];
 
     const bool stale = stamps_differ(args.check);   // acted on after the descriptor prologue
-    uint32_t cx, cy;
-    grid_cell<PACK ? kPackRowsXcd : kUnpackRowsXcd>(&cx, &cy);
-    const int32_t g = static_cast<int32_t>(cy);
-    const int32_t u0 = static_cast<int32_t>(cx) * args.units_per_wg;
+    const int32_t g = blockIdx.y;
+    const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
     const int32_t nu = min(args.units_per_wg, 2 * args.n_desc - u0);
     const int tid = threadIdx.x;
     for (int u = tid; u < nu; u += THREADS) {
@@ -84,9 +77,12 @@ __global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
         return;
     }
 
-    const uint32_t vpr = static_cast<uint32_t>(args.row_stride) / VEC;
-    const uint32_t vph = static_cast<uint32_t>(args.head_bytes) / VEC;
-    const uint32_t unit = static_cast<uint32_t>(args.block_size) * vpr;
+    // the group's staging bases, uniform: each lane selects its share's base (a per-lane index into the
+    // argument array would load it from memory inside the loop and serialise the vector loads)
+    const uint64_t st0 = args.stage[g][0], st1 = args.stage[g][1], st2 = args.stage[g][2], st3 = args.stage[g][3];
+    const uint32_t vps = args.seg_bytes / VEC;                         // vectors per share of a row
+    const uint32_t per_seg = static_cast<uint32_t>(args.block_size) * vps;
+    const uint32_t unit = static_cast<uint32_t>(args.nseg) * per_seg;
     const uint32_t total = static_cast<uint32_t>(nu) * unit;
     for (uint32_t base = tid; base < total; base += THREADS * UNROLL) {
         V r[UNROLL];
@@ -98,21 +94,20 @@ __global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
             ok[j] = false;
             dst[j] = 0;
             if (idx < total) {
+                // idx = ((unit, share), row, vector of the share)
                 const uint32_t u = fast_div(idx, args.unit_magic, args.unit_shift);
                 const uint32_t rem = idx - u * unit;
-                const uint32_t row = fast_div(rem, args.vpr_magic, args.vpr_shift);
-                const uint32_t c = rem - row * vpr;
+                const uint32_t sg = fast_div(rem, args.seg_magic, args.seg_shift);
+                const uint32_t r2 = rem - sg * per_seg;
+                const uint32_t row = fast_div(r2, args.vps_magic, args.vps_shift);
+                const uint32_t cs = r2 - row * vps;
                 if (static_cast<int32_t>(row) < s_n[u]) {
-                    const uint32_t h = fast_div(c, args.vph_magic, args.vph_shift);
-                    int32_t sg = 0;
-                    while (sg + 1 < args.nseg && h >= args.segs[sg + 1].head0) ++sg;
-                    const MergeSeg seg = args.segs[sg];
-                    const uint64_t stage = args.stage[g][sg] +
-                                           static_cast<uint64_t>(s_kv[u]) * args.total_tokens * seg.row_bytes +
-                                           static_cast<uint64_t>(s_tok[u] + row) * seg.row_bytes +
-                                           static_cast<uint64_t>(h - seg.head0) * args.head_bytes +
-                                           (c - h * vph) * VEC;
-                    const uint64_t paged = s_paged[u] + static_cast<uint64_t>(row) * args.row_stride + c * VEC;
+                    const uint64_t base = sg == 0 ? st0 : sg == 1 ? st1 : sg == 2 ? st2 : st3;
+                    const uint64_t stage = base +
+                                           static_cast<uint64_t>(s_kv[u]) * args.total_tokens * args.seg_bytes +
+                                           static_cast<uint64_t>(s_tok[u] + row) * args.seg_bytes + cs * VEC;
+                    const uint64_t paged = s_paged[u] + static_cast<uint64_t>(row) * args.row_stride +
+                                           (sg * vps + cs) * VEC;
                     const uint64_t src = PACK ? paged : stage;
                     dst[j] = PACK ? stage : paged;
                     r[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(src));

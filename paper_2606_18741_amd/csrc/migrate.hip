@@ -293,8 +293,9 @@ static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostS
 
 
 // Whole paged rows, when every layer of the call splits its rows the same way
-// into 2..kMaxMergeSegs/2 staging slices, each at least min_seg_bytes, that
-// cover all of the rank's heads.  Returns false if not applicable.
+// into 2..kMaxMergeSegs staging slices of equal head counts, each share of
+// min_seg_bytes..max_seg_bytes, that cover all of the rank's heads.  Returns
+// false if not applicable.
 template <int VEC, bool PACK>
 static void launch_rows_vec(const MergeArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small)
@@ -306,7 +307,7 @@ static void launch_rows_vec(const MergeArgs& a, dim3 grid, bool small, hipStream
 }
 
 static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t heads_per_rank, uint32_t min_seg_bytes,
-                              std::vector<std::vector<const HostSlice*>>& groups) {
+                              uint32_t max_seg_bytes, std::vector<std::vector<const HostSlice*>>& groups) {
     std::vector<int32_t> layers;
     for (const HostSlice& s : slices)
         if (std::find(layers.begin(), layers.end(), s.layer) == layers.end()) layers.push_back(s.layer);
@@ -316,10 +317,12 @@ static bool merged_rows_apply(const std::vector<HostSlice>& slices, int32_t head
         for (const HostSlice& s : slices)
             if (s.layer == l) g.push_back(&s);
         std::sort(g.begin(), g.end(), [](const HostSlice* a, const HostSlice* b) { return a->head_local < b->head_local; });
-        if (g.size() < 2 || g.size() > kMaxMergeSegs / 2) return false;
-        int32_t next = 0;                                 // slices tile the rank's heads exactly
+        if (g.size() < 2 || g.size() > static_cast<size_t>(kMaxMergeSegs)) return false;
+        int32_t next = 0;                                 // equal slices tile the rank's heads exactly
         for (const HostSlice* s : g) {
-            if (s->head_local != next || s->row_bytes < min_seg_bytes) return false;
+            if (s->head_local != next || s->row_bytes < min_seg_bytes || s->row_bytes > max_seg_bytes ||
+                s->head_count != g.front()->head_count)
+                return false;
             next += s->head_count;
         }
         if (next != heads_per_rank) return false;
@@ -338,9 +341,10 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
                                int64_t n_desc, int32_t bs, int64_t block_stride, int32_t row_stride, const char* ws,
                                int64_t desc_off, const StampCheck& check, hipStream_t stream) {
     if (groups.empty() || n_desc == 0) return REMP_OK;
-    const int64_t hb = static_cast<int64_t>(p.shape.head_dim) * p.shape.elem_bytes;
-    uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(row_stride) |
-                    static_cast<uint64_t>(hb) | 16u;
+    // merged_rows_apply admits only equal shares that tile the row: nseg * seg_bytes == row_stride
+    const int32_t nseg = static_cast<int32_t>(groups.front().size());
+    const uint32_t seg_bytes = groups.front().front()->row_bytes;
+    uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(row_stride) | seg_bytes | 16u;
     for (const auto& g : groups)
         for (const HostSlice* s : g)
             bits |= s->layer_k | s->layer_v | s->stage | s->row_bytes |
@@ -362,22 +366,19 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
     a.units_per_wg = C;
     a.row_stride = row_stride;
     a.block_size = bs;
-    a.head_bytes = static_cast<int32_t>(hb);
+    a.nseg = nseg;
+    a.seg_bytes = seg_bytes;
     a.check = check;
-    const auto& first = groups.front();
-    a.nseg = static_cast<int32_t>(first.size());
-    for (size_t i = 0; i < first.size(); ++i)
-        a.segs[i] = MergeSeg{first[i]->row_bytes, static_cast<uint16_t>(first[i]->head_local),
-                             static_cast<uint16_t>(first[i]->head_count)};
-    const FastDiv fv = make_fastdiv(static_cast<uint32_t>(row_stride / vec));
+    const uint32_t vps = seg_bytes / static_cast<uint32_t>(vec);
     const FastDiv fu = make_fastdiv(static_cast<uint32_t>(bs) * static_cast<uint32_t>(row_stride / vec));
-    const FastDiv fh = make_fastdiv(static_cast<uint32_t>(hb / vec));
-    a.vpr_magic = fv.magic;
-    a.vpr_shift = fv.shift;
+    const FastDiv fs = make_fastdiv(static_cast<uint32_t>(bs) * vps);
+    const FastDiv fv = make_fastdiv(vps);
     a.unit_magic = fu.magic;
     a.unit_shift = fu.shift;
-    a.vph_magic = fh.magic;
-    a.vph_shift = fh.shift;
+    a.seg_magic = fs.magic;
+    a.seg_shift = fs.shift;
+    a.vps_magic = fv.magic;
+    a.vps_shift = fv.shift;
     const int64_t gx = (2 * n_desc + C - 1) / C;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
@@ -794,7 +795,8 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
         return launch_tiles<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size,
                                   row_stride * sh.old_block_size, src->layout, ws, L.desc_old, check, stream);
     std::vector<std::vector<const HostSlice*>> groups;
-    if (kPackRows && merged_rows_apply(slices, plan->own_old.heads_per_rank(), kPackRowsMinSegBytes, groups))
+    if (kPackRows && merged_rows_apply(slices, plan->own_old.heads_per_rank(), kPackRowsMinShareBytes,
+                                       kPackRowsMaxShareBytes, groups))
         return launch_rows<true>(*plan, groups, plan->old_live_blocks, sh.old_block_size,
                                  row_stride * sh.old_block_size, static_cast<int32_t>(row_stride), ws, L.desc_old, check,
                                  stream);
@@ -851,7 +853,8 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
         return launch_tiles<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size,
                                    row_stride * sh.new_block_size, dst->layout, ws, L.sorted_new, check, stream);
     std::vector<std::vector<const HostSlice*>> groups;
-    if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), kMergeMinSegBytes, groups))
+    if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), kUnpackRowsMinShareBytes,
+                                        kUnpackRowsMaxShareBytes, groups))
         return launch_rows<false>(*plan, groups, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
                            static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
     return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,

@@ -182,6 +182,11 @@ remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo, c
         delete p;
         return fail(REMP_E_UNSUPPORTED, "more than 2^31 - 1 live tokens");
     }
+    // launch grids index (block, K/V) units of up to 8 slices with 32-bit workgroup ids
+    if (nb_old >= (int64_t(1) << 28) || nb_new >= (int64_t(1) << 28)) {
+        delete p;
+        return fail(REMP_E_UNSUPPORTED, "2^28 or more live blocks");
+    }
     p->total_tokens = T;
     p->old_live_blocks = nb_old;
     p->new_live_blocks = nb_new;

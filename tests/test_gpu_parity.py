@@ -211,10 +211,10 @@ EDGE = {
     "merged_rows_mha": _custom(num_layers=4, num_kv_heads=16, head_dim=128, old_topo=(4, 1), new_topo=(2, 2)),
     "merged_rows_reblock": _custom(num_layers=4, num_kv_heads=32, head_dim=128, old_topo=(8, 1),
                                    new_topo=(2, 2), old_block_size=16, new_block_size=32),
-    # several destinations split an old rank's rows into >= 1 KiB shares: pack reads whole rows
-    "pack_rows_tp2_to_tp4": _custom(num_layers=4, num_kv_heads=16, head_dim=128, old_topo=(2, 1), new_topo=(4, 1)),
-    "pack_rows_3way_reblock": _custom(num_layers=3, num_kv_heads=12, head_dim=128, old_topo=(1, 1),
-                                      new_topo=(3, 1), old_block_size=16, new_block_size=32),
+    # several destinations split an old rank's rows into 256 B shares: pack reads whole rows
+    "pack_rows_tp2_to_tp4": _custom(num_layers=4, num_kv_heads=4, head_dim=128, old_topo=(2, 1), new_topo=(4, 1)),
+    "pack_rows_4way_reblock": _custom(num_layers=3, num_kv_heads=4, head_dim=128, old_topo=(1, 1),
+                                      new_topo=(4, 1), old_block_size=16, new_block_size=32),
     "short_row_shares_fp8": _custom(num_layers=4, num_kv_heads=32, head_dim=128, elem_bytes=1,
                                     old_topo=(8, 1), new_topo=(2, 2), old_block_size=16, new_block_size=32),
     # explicit uneven pipeline partitions

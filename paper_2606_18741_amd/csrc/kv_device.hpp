@@ -76,6 +76,9 @@ constexpr uint32_t kUnpackRowsMinShareBytes = 256;
 constexpr uint32_t kPackRowsMinShareBytes = 256;
 constexpr uint32_t kPackRowsMaxShareBytes = 256;
 constexpr uint32_t kUnpackRowsMaxShareBytes = 0xFFFFFFFFu;
+// Small whole-row units (the 70B GQA unpack: 8 KiB) run one unit per 256-thread workgroup, two vectors
+// per lane (A/B on MI355X against 128 x 4: 70B unpack -1.0%; 512 x 1 and 64 x 8 slower).
+constexpr int kRowsSmallThreads = 256, kRowsSmallUnroll = 2;
 // Slices per copy launch.  Launches of a few slices beat one launch of all of them (A/B on MI355X, 70B
 // GQA share: 96 per launch 5.71, 40: 5.73, 10: 5.79-5.83, 5: 5.80, 2: 5.76, 1: 5.66 TB/s), and the kernel
 // arguments stay small.

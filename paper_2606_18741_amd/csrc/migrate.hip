@@ -299,8 +299,8 @@ static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostS
 template <int VEC, bool PACK>
 static void launch_rows_vec(const MergeArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small)
-        hipLaunchKernelGGL((copy_rows<VEC, PACK, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0, stream,
-                           a);
+        hipLaunchKernelGGL((copy_rows<VEC, PACK, kRowsSmallThreads, kRowsSmallUnroll>), grid, dim3(kRowsSmallThreads),
+                           0, stream, a);
     else
         hipLaunchKernelGGL((copy_rows<VEC, PACK, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0, stream,
                            a);

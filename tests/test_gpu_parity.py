@@ -207,7 +207,8 @@ EDGE = {
     "replicated_tp16_to_tp8pp2": _custom(num_layers=8, num_kv_heads=4, head_dim=64, old_topo=(16, 1),
                                          new_topo=(8, 2), old_block_size=16, new_block_size=32),
     "replicated_keep_local": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(8, 1), new_topo=(4, 2)),
-    # several sources fill each new row with >= 1 KiB shares: unpack writes whole rows
+    # several sources fill each new row with equal shares of >= 256 B: unpack writes whole rows (the fp8 case
+    # below has four 512 B shares; heads_not_nested_reblock has unequal shares and takes per-slice copies)
     "merged_rows_mha": _custom(num_layers=4, num_kv_heads=16, head_dim=128, old_topo=(4, 1), new_topo=(2, 2)),
     "merged_rows_reblock": _custom(num_layers=4, num_kv_heads=32, head_dim=128, old_topo=(8, 1),
                                    new_topo=(2, 2), old_block_size=16, new_block_size=32),

@@ -363,13 +363,24 @@ def _layout_workload(shape):
 @pytest.mark.parametrize("lo,ln", LAYOUT_CASES)
 @pytest.mark.parametrize("shape", ["gqa70b", "mha7b_reblock", "fp8", "replicated"])
 def test_layouts(shape, lo, ln):
+    _layouts_case(shape, lo, ln, reuse=False)
+
+
+@pytest.mark.parametrize("lo,ln", [(1, 2), (2, 1)])
+@pytest.mark.parametrize("shape", ["gqa70b", "mha7b_reblock"])
+def test_layouts_reuse(shape, lo, ln):
+    """Head-tile copies with descriptors reused after the first pack and the first unpack."""
+    _layouts_case(shape, lo, ln, reuse=True)
+
+
+def _layouts_case(shape, lo, ln, reuse):
     rk = _rk()
     w = _layout_workload(shape)
     inp = synthkv.make_inputs(w)
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables)
     new_host = hostpools.sentinel_pools(w, inp.new_tables)
-    log(f"[layout] {shape} old {lo} new {ln}")
+    log(f"[layout] {shape} old {lo} new {ln} reuse {reuse}")
     plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
     W_old, W_new = plan.info.old_world, plan.info.new_world
     dto, dtn = DeviceTables(inp.old_tables), DeviceTables(inp.new_tables)
@@ -380,12 +391,13 @@ def test_layouts(shape, lo, ln):
     pairs = [(p.src, p.dst) for p in plan.pairs]
     staging = staging_for_pairs(plan, w.seed, pairs)
     ws = Workspace(plan)
+    ru = rk.REMP_KV_REUSE_DESCRIPTORS if reuse else 0
     for r in range(W_old):
         plan.pack(r, src[r][0], dto.dev, window_args(plan, staging, r, W_new, True, 0, L), ws.buf, ws.bytes,
-                  stream_handle())
+                  stream_handle(), flags=ru if r else 0)
     for q in range(W_new):
         plan.unpack(q, window_args(plan, staging, q, W_old, False, 0, L), dst[q][0], dtn.host, dtn.dev, ws.buf,
-                    ws.bytes, stream_handle())
+                    ws.bytes, stream_handle(), flags=ru if q else 0)
     torch.cuda.synchronize()
     assert ws.flag() == 0
     st = oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables,
@@ -412,13 +424,24 @@ def test_layouts(shape, lo, ln):
 def test_local_fast_path_layouts(shape, lo, ln):
     """Local fast path with HND / ROCm pools: pack and unpack skip the local slices, copy_local moves them
     through head tiles; every byte of every new pool must equal the oracle's, in the new layout."""
+    _local_layouts_case(shape, lo, ln, reuse=False)
+
+
+@pytest.mark.parametrize("lo,ln", [(1, 2), (2, 1), (1, 1)])
+@pytest.mark.parametrize("shape", ["gqa70b", "replicated"])
+def test_local_fast_path_layouts_reuse(shape, lo, ln):
+    """The same with the block descriptors reused by every call after the first pack and unpack."""
+    _local_layouts_case(shape, lo, ln, reuse=True)
+
+
+def _local_layouts_case(shape, lo, ln, reuse):
     rk = _rk()
     w = _layout_workload(shape)
     inp = synthkv.make_inputs(w)
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables)
     new_host = hostpools.sentinel_pools(w, inp.new_tables)
-    log(f"[local layout] {shape} old {lo} new {ln}")
+    log(f"[local layout] {shape} old {lo} new {ln} reuse {reuse}")
     plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
     W_old, W_new = plan.info.old_world, plan.info.new_world
     dto, dtn = DeviceTables(inp.old_tables), DeviceTables(inp.new_tables)
@@ -430,18 +453,20 @@ def test_local_fast_path_layouts(shape, lo, ln):
     staging = staging_for_pairs(plan, w.seed, pairs)
     ws = Workspace(plan)
     fl = rk.REMP_KV_SKIP_LOCAL
+    ru = rk.REMP_KV_REUSE_DESCRIPTORS if reuse else 0
     for r in range(W_old):
         plan.pack(r, src[r][0], dto.dev, window_args(plan, staging, r, W_new, True, 0, L), ws.buf, ws.bytes,
-                  stream_handle(), flags=fl)
+                  stream_handle(), flags=fl | (ru if r else 0))
     torch.cuda.synchronize()
     assert ws.flag() == 0
     for q in range(W_new):
         plan.unpack(q, window_args(plan, staging, q, W_old, False, 0, L), dst[q][0], dtn.host, dtn.dev, ws.buf,
-                    ws.bytes, stream_handle(), flags=fl)
+                    ws.bytes, stream_handle(), flags=fl | (ru if q else 0))
     torch.cuda.synchronize()
     assert ws.flag() == 0
     for r in range(min(W_old, W_new)):
-        plan.copy_local(r, src[r][0], dto.dev, dst[r][0], dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle())
+        plan.copy_local(r, src[r][0], dto.dev, dst[r][0], dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle(),
+                        flags=ru)
     torch.cuda.synchronize()
     assert ws.flag() == 0
     oracle.reshard(old_host, new_host, T(*w.old_topo), T(*w.new_topo), L, H, inp.old_tables, inp.new_tables)
@@ -516,6 +541,15 @@ def _unchanged(staging, before, dst, new_host, elem_bytes):
 
 @pytest.mark.parametrize("fill", ["zeros", "random"])
 def test_reuse_without_expansion_copies_nothing(fill):
+    _reuse_stale_case(fill, layout=0)
+
+
+def test_reuse_without_expansion_copies_nothing_hnd():
+    """The same for head-tile kernels (HND pools)."""
+    _reuse_stale_case("random", layout=1)
+
+
+def _reuse_stale_case(fill, layout):
     """A reusing call on a workspace that holds no matching descriptors copies nothing and sets flag 2."""
     rk = _rk()
     w = synthkv.reduced(synthkv.TINY, num_seqs=4, max_len=120)
@@ -532,18 +566,21 @@ def test_reuse_without_expansion_copies_nothing(fill):
     else:
         ws.buf.zero_()
     reuse = rk.REMP_KV_REUSE_DESCRIPTORS
-    log(f"[reuse] no expansion, workspace {fill}")
-    plan.pack(0, src[0].arg, dto.dev, window_args(plan, staging, 0, plan.info.new_world, True, 0, L), ws.buf,
+    # the same storage read as `layout` (HND selects the head-tile kernels; nothing may be written anyway)
+    src_arg = rk.PoolArg(list(src[0].arg._k), list(src[0].arg._v), inp.old_tables.num_blocks, layout=layout)
+    dst_arg = rk.PoolArg(list(dst[0].arg._k), list(dst[0].arg._v), inp.new_tables.num_blocks, layout=layout)
+    log(f"[reuse] no expansion, workspace {fill}, layout {layout}")
+    plan.pack(0, src_arg, dto.dev, window_args(plan, staging, 0, plan.info.new_world, True, 0, L), ws.buf,
               ws.bytes, stream_handle(), flags=reuse)
     torch.cuda.synchronize()
     assert ws.flag() == 2
     ws.set_flag(0)
-    plan.unpack(0, window_args(plan, staging, 0, plan.info.old_world, False, 0, L), dst[0].arg, dtn.host, dtn.dev,
+    plan.unpack(0, window_args(plan, staging, 0, plan.info.old_world, False, 0, L), dst_arg, dtn.host, dtn.dev,
                 ws.buf, ws.bytes, stream_handle(), flags=reuse)
     torch.cuda.synchronize()
     assert ws.flag() == 2
     ws.set_flag(0)
-    plan.copy_local(0, src[0].arg, dto.dev, dst[0].arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle(),
+    plan.copy_local(0, src_arg, dto.dev, dst_arg, dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle(),
                     flags=reuse)
     torch.cuda.synchronize()
     assert ws.flag() == 2

@@ -554,6 +554,18 @@ static remp_status collect_slices(const remp_kv_plan_t& p, bool pack, int32_t ra
     return REMP_OK;
 }
 
+// In an HND pool the rows of one head's tile are contiguous and in token
+// order, so a slice of a single head has the staging slice's byte order: it is
+// copied like an NHD slice whose rows are one head long.  Used for pack (A/B
+// on MI355X, 70B GQA share with HND pools: pack -4.3% time against the LDS
+// tile kernel); the unpack keeps the tile kernel (+1.2% with the direct copy).
+static bool hnd_single_heads(int32_t layout, const std::vector<HostSlice>& slices) {
+    if (layout != kLayoutHND) return false;
+    for (const HostSlice& s : slices)
+        if (s.head_count != 1) return false;
+    return true;
+}
+
 // ---------------------------------------------------------------------------
 // local copy: old pool -> new pool for slices that stay on the same rank
 // ---------------------------------------------------------------------------
@@ -791,6 +803,11 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
                                               true, stream, -1, old_at, old_stamp(*plan))) {
         return st;
     }
+    if (hnd_single_heads(src->layout, slices))
+        return launch_copy<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size,
+                                 row_stride * sh.old_block_size,
+                                 static_cast<int32_t>(row_stride / plan->own_old.heads_per_rank()), ws, L.desc_old,
+                                 check, stream);
     if (src->layout != kLayoutNHD)
         return launch_tiles<true>(*plan, slices, plan->old_live_blocks, sh.old_block_size,
                                   row_stride * sh.old_block_size, src->layout, ws, L.desc_old, check, stream);

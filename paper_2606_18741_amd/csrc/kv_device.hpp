@@ -103,7 +103,12 @@ constexpr int64_t kSmallWgBytes = 4 * 1024;
 // 70B GQA -4.7% time, long context -5.8%, Qwen3-30B-A3B -5.6% (DeepSeek-32B -3.6% without the
 // prewarm); 256 threads or 32 KiB were slower (8 KiB against 4 KiB had been +14%).
 constexpr int64_t kLocalSmallWgBytes = 16 * 1024;
-constexpr int kLargeThreads = 256, kLargeUnroll = 8;
+// Large units (MHA rows of 2 KiB and more): 16-wave workgroups with two loads in flight per lane,
+// against 4 waves with eight (MI355X, one process, three repetitions): 7B MHA step -3.4%, 13B MHA
+// pack -2.1% and unpack -2.9% time.  The local copy's optimum differs: 512 x 4 was faster than
+// 256 x 8 on both shapes (7B -4%, 13B -2.8%), 1024 x 2 -10.7% on 7B but +0.8% on 13B.
+constexpr int kLargeThreads = 1024, kLargeUnroll = 2;
+constexpr int kLocalLargeThreads = 512, kLocalLargeUnroll = 4;
 constexpr int64_t kLargeWgBytes = 64 * 1024;
 constexpr int kScanThreads = 1024;
 

@@ -580,7 +580,8 @@ static remp_status launch_local_vec(const LocalArgs& a, dim3 grid, bool small, h
     if (small)
         hipLaunchKernelGGL((copy_local<VEC, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL((copy_local<VEC, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0, stream, a);
+        hipLaunchKernelGGL((copy_local<VEC, kLocalLargeThreads, kLocalLargeUnroll>), grid, dim3(kLocalLargeThreads), 0,
+                           stream, a);
     return hip_check(hipGetLastError(), "copy_local launch");
 }
 

@@ -109,6 +109,9 @@ constexpr int64_t kLocalSmallWgBytes = 16 * 1024;
 // 256 x 8 on both shapes (7B -4%, 13B -2.8%), 1024 x 2 -10.7% on 7B but +0.8% on 13B.
 constexpr int kLargeThreads = 1024, kLargeUnroll = 2;
 constexpr int kLocalLargeThreads = 512, kLocalLargeUnroll = 4;
+// and at most 32 KiB per workgroup (7B MHA copy_local -5% against 64 KiB; 13B MHA, whose 40 KiB units
+// go one per workgroup either way, unchanged)
+constexpr int64_t kLocalLargeWgBytes = 32 * 1024;
 constexpr int64_t kLargeWgBytes = 64 * 1024;
 constexpr int kScanThreads = 1024;
 

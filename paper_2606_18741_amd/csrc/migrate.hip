@@ -688,7 +688,7 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     const int vec = static_cast<int>(bits & (~bits + 1));
     const int64_t per_unit = static_cast<int64_t>(bn) * max_row;
     const bool small = per_unit <= kSmallUnitBytes;
-    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kLocalSmallWgBytes : kLargeWgBytes));
+    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kLocalSmallWgBytes : kLocalLargeWgBytes));
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
     C = std::min<int32_t>(C, std::max<int32_t>(1, kMaxLocalRows / bn));
     if (bn > kMaxLocalRows) return fail(REMP_E_UNSUPPORTED, "new block size above the local-copy row limit");

@@ -320,6 +320,19 @@ def test_local_fast_path_windows():
     check_against_oracle(w, synthkv.make_inputs(w), windows=[(0, 13), (13, 40), (40, 80)], local=True)
 
 
+@pytest.mark.parametrize("wg_bytes", [2048, 8192, 32768, 262144, 1 << 20])
+@pytest.mark.parametrize("name", ["mha7b", "gqa70b", "merged_rows_mha"])
+def test_workgroup_sizes(name, wg_bytes, monkeypatch):
+    """Bit-exact at other bytes-per-workgroup targets (REMP_KV_WG_BYTES, a tuning override): one to
+    many units per workgroup and ragged last workgroups, for the small-unit (GQA) and large-unit (MHA)
+    launch shapes, staged and with the local fast path."""
+    w = EDGE[name] if name in EDGE else synthkv.reduced(synthkv.WORKLOADS[name], num_seqs=4, max_len=250)
+    monkeypatch.setenv("REMP_KV_WG_BYTES", str(wg_bytes))
+    inp = synthkv.make_inputs(w)
+    check_against_oracle(w, inp, log_name=f"{name} wg {wg_bytes}")
+    check_against_oracle(w, inp, log_name=f"{name} wg {wg_bytes} local", local=True)
+
+
 # ---------------------------------------------------------------------------
 # pool layouts: HND and the ROCm paged-attention layout go through LDS tiles
 # ---------------------------------------------------------------------------

@@ -117,7 +117,7 @@ struct LocalArgs {
 };
 static_assert(sizeof(LocalArgs) < 4096, "local copy kernel arguments must stay below 4 KiB");
 
-template <int VEC, int THREADS, int UNROLL>
+template <int VEC, int THREADS, int UNROLL, bool XCD>
 __global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
     typedef typename VecT<VEC>::type V;
     __shared__ uint64_t s_dst[kMaxUnitsPerWg];
@@ -125,8 +125,10 @@ __global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
     __shared__ uint64_t s_src[kMaxLocalRows];
 
     if (stale_descriptors(args.check)) return;
-    const LocalItem& it = args.items[blockIdx.y];
-    const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
+    uint32_t cx, cy;
+    grid_cell<XCD>(&cx, &cy);
+    const LocalItem& it = args.items[cy];
+    const int32_t u0 = static_cast<int32_t>(cx) * args.units_per_wg;
     const int32_t nu = min(args.units_per_wg, 2 * args.n_new_desc - u0);
     const int tid = threadIdx.x;
     const int32_t bn = args.new_block_size, bo = args.old_block_size;

@@ -49,7 +49,7 @@ struct MergeArgs {
 };
 static_assert(sizeof(MergeArgs) < 4096, "whole-row kernel arguments must stay below 4 KiB");
 
-template <int VEC, bool PACK, int THREADS, int UNROLL>
+template <int VEC, bool PACK, int THREADS, int UNROLL, bool XCD>
 __global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
     typedef typename VecT<VEC>::type V;
     __shared__ uint64_t s_paged[kMaxUnitsPerWg];
@@ -58,8 +58,10 @@ __global__ __launch_bounds__(THREADS) void copy_rows(const MergeArgs args) {
     __shared__ int32_t s_kv[kMaxUnitsPerWg];
 
     const bool stale = stamps_differ(args.check);   // acted on after the descriptor prologue
-    const int32_t g = blockIdx.y;
-    const int32_t u0 = static_cast<int32_t>(blockIdx.x) * args.units_per_wg;
+    uint32_t cx, cy;
+    grid_cell<XCD>(&cx, &cy);
+    const int32_t g = static_cast<int32_t>(cy);
+    const int32_t u0 = static_cast<int32_t>(cx) * args.units_per_wg;
     const int32_t nu = min(args.units_per_wg, 2 * args.n_desc - u0);
     const int tid = threadIdx.x;
     for (int u = tid; u < nu; u += THREADS) {

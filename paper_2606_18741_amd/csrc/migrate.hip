@@ -299,10 +299,10 @@ static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostS
 template <int VEC, bool PACK>
 static void launch_rows_vec(const MergeArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small)
-        hipLaunchKernelGGL((copy_rows<VEC, PACK, kRowsSmallThreads, kRowsSmallUnroll>), grid, dim3(kRowsSmallThreads),
+        hipLaunchKernelGGL((copy_rows<VEC, PACK, kRowsSmallThreads, kRowsSmallUnroll, false>), grid, dim3(kRowsSmallThreads),
                            0, stream, a);
     else
-        hipLaunchKernelGGL((copy_rows<VEC, PACK, kLargeThreads, kLargeUnroll>), grid, dim3(kLargeThreads), 0, stream,
+        hipLaunchKernelGGL((copy_rows<VEC, PACK, kLargeThreads, kLargeUnroll, kRowsLargeXcd>), grid, dim3(kLargeThreads), 0, stream,
                            a);
 }
 
@@ -578,9 +578,9 @@ struct HostLocal {
 template <int VEC>
 static remp_status launch_local_vec(const LocalArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small)
-        hipLaunchKernelGGL((copy_local<VEC, kSmallThreads, kSmallUnroll>), grid, dim3(kSmallThreads), 0, stream, a);
+        hipLaunchKernelGGL((copy_local<VEC, kSmallThreads, kSmallUnroll, false>), grid, dim3(kSmallThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL((copy_local<VEC, kLocalLargeThreads, kLocalLargeUnroll>), grid, dim3(kLocalLargeThreads), 0,
+        hipLaunchKernelGGL((copy_local<VEC, kLocalLargeThreads, kLocalLargeUnroll, kLocalLargeXcd>), grid, dim3(kLocalLargeThreads), 0,
                            stream, a);
     return hip_check(hipGetLastError(), "copy_local launch");
 }

@@ -41,3 +41,21 @@ def random_windows(seed: int, L: int):
     cuts = sorted(int(c) for c in rng.choice(np.arange(1, L), k, replace=False)) if L > 1 and k else []
     b = [0] + cuts + [L]
     return list(zip(b[:-1], b[1:]))
+
+
+LAYOUT_PAIRS = [(1, 1), (1, 2), (2, 1), (2, 2), (0, 1), (1, 0), (0, 2), (2, 0)]
+
+
+def layout_cases(n: int, start: int = 40):
+    """(seed, old layout, new layout) for the first n seeds from `start` whose shapes the head-tile
+    layouts take (16-byte head rows; for the ROCm layout 16-byte block columns too); the layout pair of
+    a seed is drawn from its own stream.  Layouts: 0 NHD, 1 HND, 2 ROCm."""
+    out, seed = [], start
+    while len(out) < n and seed < start + 20 * n:
+        w = random_workload(seed)
+        lo, ln = LAYOUT_PAIRS[np.random.default_rng(3000 + seed).integers(len(LAYOUT_PAIRS))]
+        rocm_ok = all((bs * w.elem_bytes) % 16 == 0 for bs in (w.old_block_size, w.new_block_size))
+        if (w.head_dim * w.elem_bytes) % 16 == 0 and (2 not in (lo, ln) or rocm_ok):
+            out.append((seed, lo, ln))
+        seed += 1
+    return out

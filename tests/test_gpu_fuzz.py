@@ -6,15 +6,16 @@ change across the switch, empty and fragmented pools, and layer windows are
 drawn at random (tests/fuzzcases.py); every case runs the staged path over
 random layer windows and the local fast path, and (half the seeds each)
 the staged or the local path over random windows with the block
-descriptors expanded once and reused by every later call.
+descriptors expanded once and reused by every later call.  A second set
+of seeds runs on HND and ROCm pools (random layout pairs), staged and local.
 """
 from __future__ import annotations
 
 import pytest
 
 import synthkv
-from fuzzcases import random_windows, random_workload
-from test_gpu_parity import check_against_oracle
+from fuzzcases import layout_cases, random_windows, random_workload
+from test_gpu_parity import _layouts_case, _local_layouts_case, check_against_oracle
 
 pytestmark = pytest.mark.gpu
 
@@ -31,3 +32,10 @@ def test_random_configuration(seed):
     check_against_oracle(w, inp, local=True, log_name=f"fuzz{seed} local")
     check_against_oracle(w, inp, windows=random_windows(seed + 1000, w.num_layers), local=bool(seed % 2),
                          reuse=True, log_name=f"fuzz{seed} reuse")
+
+
+@pytest.mark.parametrize("seed,lo,ln", layout_cases(20))
+def test_random_configuration_layouts(seed, lo, ln):
+    w = random_workload(seed)
+    _layouts_case(w, lo, ln, reuse=bool(seed % 2))
+    _local_layouts_case(w, lo, ln, reuse=seed % 3 == 0)

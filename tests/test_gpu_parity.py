@@ -387,8 +387,10 @@ def test_layouts_reuse(shape, lo, ln):
 
 
 def _layouts_case(shape, lo, ln, reuse):
+    """shape: a name of _layout_workload, or a workload."""
     rk = _rk()
-    w = _layout_workload(shape)
+    w = shape if isinstance(shape, synthkv.KVWorkload) else _layout_workload(shape)
+    shape = shape if isinstance(shape, str) else w.name
     inp = synthkv.make_inputs(w)
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables)
@@ -448,8 +450,10 @@ def test_local_fast_path_layouts_reuse(shape, lo, ln):
 
 
 def _local_layouts_case(shape, lo, ln, reuse):
+    """shape: a name of _layout_workload, or a workload."""
     rk = _rk()
-    w = _layout_workload(shape)
+    w = shape if isinstance(shape, synthkv.KVWorkload) else _layout_workload(shape)
+    shape = shape if isinstance(shape, str) else w.name
     inp = synthkv.make_inputs(w)
     L, H = w.num_layers, w.num_kv_heads
     old_host = hostpools.source_pools(w, inp.old_tables)

@@ -12,8 +12,8 @@
  *   2. packs, on the GPU, an old rank's live paged K/V rows into one contiguous
  *      staging buffer per destination rank;
  *   3. unpacks, on the GPU, the staging buffers a new rank receives into its
- *      paged pool under the new block tables (the deterministic block remapping
- *      of Section 3.4.5; the block size may change).
+ *      paged pool under the new block tables (the new tables are the block
+ *      remapping that Section 3.4.5 allows; the block size may change).
  *
  * The transfer of staging buffers between GPUs (Section 3.4.3) is the
  * caller's: on one GPU the buffers simply stay in that GPU's memory.
@@ -110,9 +110,13 @@ typedef struct {
 
 /* The same three arrays in device memory (the GPU copy a serving engine keeps
  * for its attention kernels).  The contents must equal the host tables given
- * for the same role; the kernels bound every access by the host sizes, so a
- * mismatch cannot make them read or write outside the buffers, and it is
- * reported through the workspace flag (see remp_kv_workspace_bytes). */
+ * for the same role.  The kernels bound every access by the host sizes, so a
+ * mismatch cannot make them read or write outside their buffers.  Device
+ * tables that would index out of range (a negative length, a row or block id
+ * outside the host sizes, more tokens than planned, a token with no old
+ * source) are reported through the workspace flag (see
+ * remp_kv_workspace_bytes); device tables that stay in range but differ from
+ * the host tables are not detected, and then move other rows. */
 typedef struct {
     const int32_t* seq_lens;
     const int32_t* row_offsets;
@@ -205,7 +209,13 @@ enum {
  * (REMP_E_UNSUPPORTED), table structure (REMP_E_INVALID) and old block ids in
  * [0, old_tables->num_blocks) (REMP_E_RANGE); at most 2^31 - 1 live tokens and
  * fewer than 2^28 live blocks in either block size (REMP_E_UNSUPPORTED).  On
- * failure *out is NULL. */
+ * failure *out is NULL.
+ * Tuning hook (measurement only): if the environment variable
+ * REMP_KV_WG_BYTES holds a positive integer when the plan is created, the copy
+ * kernels launched with this plan aim to move about that many bytes per
+ * workgroup instead of the built-in per-kernel targets (capped at 1 GiB).  It
+ * changes launch shapes only, never the bytes written; later changes of the
+ * environment do not affect an existing plan. */
 REMP_API remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo,
                          const remp_kv_shape* shape, const remp_block_tables* old_tables,
                          remp_kv_plan_t** out);
@@ -229,10 +239,12 @@ REMP_API remp_status remp_kv_plan_query(const remp_kv_plan_t* plan, int32_t src,
  * remp_kv_copy_local with this plan.  The workspace is device memory, 256-byte
  * aligned, owned by the caller; calls that share one must be ordered (one
  * stream).  After the stream work of a call that expands the tables completes,
- * its first 4 bytes (int32) hold 0 if the device tables agreed with the host
- * tables and 1 otherwise; 2 means a call with REMP_KV_REUSE_DESCRIPTORS found
- * no matching descriptors and copied nothing.  Bytes 8-23 hold the stamps of
- * the descriptors; the rest is scratch space of the kernels. */
+ * its first 4 bytes (int32) hold 1 if the device tables would have made a
+ * kernel index out of range (the cases listed at remp_dev_tables; those
+ * accesses were skipped) and 0 otherwise; 2 means a call with
+ * REMP_KV_REUSE_DESCRIPTORS found no matching descriptors and copied nothing.
+ * Bytes 8-23 hold the stamps of the descriptors; the rest is scratch space of
+ * the kernels. */
 REMP_API remp_status remp_kv_workspace_bytes(const remp_kv_plan_t* plan, int64_t* bytes);
 
 /* Pack (Section 3.4.2 send side, Section 3.4.3): for every slice old_rank sends

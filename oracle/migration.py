@@ -29,7 +29,7 @@ Readings of points the paper leaves open:
   sits in block table[s][t // block_size], slot t % block_size; only live
   tokens (t < n_s) are payload;
 * the block mapping across the switch is the caller's new block tables (the
-  "deterministic block remapping" of Section 3.4.5); the new block size may
+  remapping of block identities that Section 3.4.5 permits); the new block size may
   differ from the old one;
 * K and V are two arrays moved identically;
 * staging, the contiguous buffer an old rank r fills for a new rank q: the
@@ -100,14 +100,6 @@ def tp_owners(h: int, topo: Topology, H: int) -> List[int]:
     return list(range(h * rep, (h + 1) * rep))
 
 
-def tp_owner(h: int, topo: Topology, H: int) -> int:
-    """The tensor rank that holds KV head h (topologies without replication)."""
-    owners = tp_owners(h, topo, H)
-    if len(owners) != 1:
-        raise ValueError("head is replicated in this topology")
-    return owners[0]
-
-
 def rank_of(pp: int, tp: int, topo: Topology) -> int:
     """Global rank of (pipeline stage, tensor rank)."""
     return pp * topo.tp + tp
@@ -116,11 +108,6 @@ def rank_of(pp: int, tp: int, topo: Topology) -> int:
 def holders(l: int, h: int, topo: Topology, L: int, H: int) -> List[int]:
     """Global ranks holding (layer l, head h): rank(l, h, T) of Section 3.4.1, as a set."""
     return [rank_of(pp_owner(l, topo, L), t, topo) for t in tp_owners(h, topo, H)]
-
-
-def owner(l: int, h: int, topo: Topology, L: int, H: int) -> int:
-    """rank(l, h, T) for a topology without replication."""
-    return rank_of(pp_owner(l, topo, L), tp_owner(h, topo, H), topo)
 
 
 def source_of(l: int, h: int, q: int, old: Topology, new: Topology, L: int, H: int) -> int:

@@ -145,10 +145,12 @@ __global__ __launch_bounds__(THREADS) void copy_local(const LocalArgs args) {
         const BlockDesc d = args.new_desc[g >> 1];
         uint64_t a = 0;
         if (r < d.n) {
-            const int32_t t = d.tok - args.tok_off[d.seq] + r;          // token within its sequence
+            // token within its sequence: the new expansion's token offset less the old one's, so
+            // device tables that disagree can make it negative; such a row has no source
+            const int32_t t = d.tok - args.tok_off[d.seq] + r;
             const int32_t ob = args.old_blk_off[d.seq] + t / bo;
             const int32_t slot = t - (t / bo) * bo;
-            bool ok = ob >= 0 && ob < args.n_old_desc;
+            bool ok = t >= 0 && ob >= 0 && ob < args.n_old_desc;
             BlockDesc od{0, 0, 0, 0};
             if (ok) {
                 od = args.old_desc[ob];

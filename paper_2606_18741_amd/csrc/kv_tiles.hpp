@@ -306,10 +306,11 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
         uint64_t base = 0;
         int32_t slot = 0;
         if (r < nd.n) {
-            const int32_t t = nd.tok - a.tok_off[nd.seq] + r;            // token within its sequence
+            // token within its sequence (negative when the device tables disagree: no source)
+            const int32_t t = nd.tok - a.tok_off[nd.seq] + r;
             const int32_t ob = a.old_blk_off[nd.seq] + t / bo;
             slot = t - (t / bo) * bo;
-            bool ok = ob >= 0 && ob < a.n_old_desc;
+            bool ok = t >= 0 && ob >= 0 && ob < a.n_old_desc;
             BlockDesc od{0, 0, 0, 0};
             if (ok) {
                 od = a.old_desc[ob];

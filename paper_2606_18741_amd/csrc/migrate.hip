@@ -40,11 +40,9 @@ namespace remp {
 static thread_local hipEvent_t g_trace_start = nullptr;
 static thread_local hipEvent_t g_trace_stop = nullptr;
 
-static int env_int(const char* name, int dflt) {
-    const char* v = std::getenv(name);
-    if (!v || !*v) return dflt;
-    return std::atoi(v);
-}
+// Bytes a copy workgroup aims to move: the built-in target of the launch kind, or the plan's
+// tuning override (REMP_KV_WG_BYTES when the plan was created).
+static int64_t wg_target(const remp_kv_plan_t& p, int64_t builtin) { return p.wg_bytes > 0 ? p.wg_bytes : builtin; }
 
 struct HostSlice {
     uint64_t paged_k, paged_v, stage;
@@ -72,11 +70,11 @@ static uint64_t finish64(uint64_t z) {
 
 static uint64_t old_stamp(const remp_kv_plan_t& p) { return finish64(mix64(mix64(0, p.serial), 1)); }
 
-static StampCheck no_check(char* ws) {
+static StampCheck no_check(int32_t* flag) {
     StampCheck c;
     c.at[0] = c.at[1] = nullptr;
     c.want[0] = c.want[1] = 0;
-    c.flag = reinterpret_cast<int32_t*>(ws);
+    c.flag = flag;
     return c;
 }
 
@@ -84,16 +82,16 @@ static uint32_t sort_buckets(int64_t n_desc) {
     return static_cast<uint32_t>((std::max<int64_t>(n_desc, 1) + kDescsPerBucket - 1) / kDescsPerBucket);
 }
 
-// Enqueue expansion of `tables` into the workspace areas at scan_off / desc_off.
-// With bucket_off >= 0 the expansion also clears and fills the bucket counters
-// of the descriptor sort (new tables only).  A non-NULL stamp_at receives
-// `stamp` in the same launch that writes the descriptors.
+// Enqueue expansion of `tables` into the workspace areas at scan_off / desc_off;
+// `flag` is the status flag (reset first if reset_flag).  With bucket_off >= 0
+// the expansion also clears and fills the bucket counters of the descriptor
+// sort (new tables only).  A non-NULL stamp_at receives `stamp` in the same
+// launch that writes the descriptors.
 static remp_status launch_expand(const remp_kv_plan_t& p, const remp_dev_tables& dt, int32_t bs, int64_t nnz,
-                                 int64_t num_blocks, int64_t n_desc, char* ws, int64_t scan_off, int64_t desc_off,
-                                 bool reset_flag, hipStream_t stream, int64_t bucket_off, uint64_t* stamp_at,
-                                 uint64_t stamp) {
+                                 int64_t num_blocks, int64_t n_desc, char* ws, int32_t* flag, int64_t scan_off,
+                                 int64_t desc_off, bool reset_flag, hipStream_t stream, int64_t bucket_off,
+                                 uint64_t* stamp_at, uint64_t stamp) {
     if (n_desc >= (int64_t(1) << 30)) return fail(REMP_E_UNSUPPORTED, "more than 2^30 live blocks in one call");
-    int32_t* flag = reinterpret_cast<int32_t*>(ws);
     int32_t* tok_off = reinterpret_cast<int32_t*>(ws + scan_off);
     int32_t* blk_off = tok_off + (p.num_seqs + 1);
     BlockDesc* desc = reinterpret_cast<BlockDesc*>(ws + desc_off);
@@ -171,7 +169,7 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     const int vec = static_cast<int>(bits & (~bits + 1));   // lowest set bit, <= 16
     const int64_t per_unit = static_cast<int64_t>(bs) * max_row;
     const bool small = per_unit <= kSmallUnitBytes;
-    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kSmallWgBytes : kLargeWgBytes));
+    const int64_t target = wg_target(p, small ? kSmallWgBytes : kLargeWgBytes);
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
     // the flattened per-workgroup index must stay below 2^32
     while (C > 1 && static_cast<uint64_t>(C) * bs * (max_row / vec) >= (uint64_t(1) << 32)) C >>= 1;
@@ -352,7 +350,7 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
     const int vec = static_cast<int>(bits & (~bits + 1));
     const int64_t per_unit = static_cast<int64_t>(bs) * row_stride;
     const bool small = per_unit <= kSmallUnitBytes;
-    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kSmallWgBytes : kLargeWgBytes));
+    const int64_t target = wg_target(p, small ? kSmallWgBytes : kLargeWgBytes);
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
     while (C > 1 && static_cast<uint64_t>(C) * bs * (row_stride / vec) >= (uint64_t(1) << 32)) C >>= 1;
     if (static_cast<uint64_t>(bs) * (row_stride / vec) >= (uint64_t(1) << 32))
@@ -688,7 +686,7 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     const int vec = static_cast<int>(bits & (~bits + 1));
     const int64_t per_unit = static_cast<int64_t>(bn) * max_row;
     const bool small = per_unit <= kSmallUnitBytes;
-    const int64_t target = env_int("REMP_KV_WG_BYTES", static_cast<int>(small ? kLocalSmallWgBytes : kLocalLargeWgBytes));
+    const int64_t target = wg_target(p, small ? kLocalSmallWgBytes : kLocalLargeWgBytes);
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
     C = std::min<int32_t>(C, std::max<int32_t>(1, kMaxLocalRows / bn));
     if (bn > kMaxLocalRows) return fail(REMP_E_UNSUPPORTED, "new block size above the local-copy row limit");
@@ -752,6 +750,67 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
 
 static bool ranges_overlap(uint64_t a, uint64_t an, uint64_t b, uint64_t bn) { return a < b + bn && b < a + an; }
 
+// Argument checks shared by the unpack entry points (everything but the workspace and the tables).
+static remp_status check_unpack_args(const remp_kv_plan_t* plan, int32_t new_rank, int32_t layer_begin,
+                                     int32_t layer_end, const remp_buffer* staging, const remp_kv_pool* dst,
+                                     uint32_t flags) {
+    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL | REMP_KV_REUSE_DESCRIPTORS))
+        return fail(REMP_E_INVALID, "unknown flags");
+    if (new_rank < 0 || new_rank >= plan->own_new.world())
+        return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
+                                      std::to_string(plan->own_new.world()) + ")");
+    if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
+    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_of_rank(new_rank), plan->shape.new_block_size,
+                                    "destination"))
+        return st;
+    if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
+    return REMP_OK;
+}
+
+// Unpack with its scratch areas at `ws` (laid out by workspace_layout) and the status flag at `flag`.
+static remp_status unpack_impl(const remp_kv_plan_t* plan, int32_t new_rank, int32_t layer_begin, int32_t layer_end,
+                               const remp_buffer* staging, const remp_kv_pool* dst,
+                               const remp_block_tables* new_tables, const remp_dev_tables* new_dev_tables, char* ws,
+                               int32_t* flag, uint32_t flags, hipStream_t stream) {
+    int64_t nnz = 0;
+    uint64_t new_stamp = 0;
+    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz, &new_stamp)) return st;
+    if (remp_status st = check_dev_tables(plan, new_dev_tables, nnz, "new")) return st;
+
+    std::vector<HostSlice> slices;
+    if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging,
+                                        (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
+        return st;
+    if (layer_begin == layer_end || plan->new_live_blocks == 0) return REMP_OK;   // as in pack
+    const remp_kv_shape& sh = plan->shape;
+    const int64_t row_stride = static_cast<int64_t>(plan->own_new.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
+    const WorkspaceLayout L = workspace_layout(*plan);
+    uint64_t* new_at = reinterpret_cast<uint64_t*>(ws + L.stamp_new);
+    StampCheck check = no_check(flag);
+    if (flags & REMP_KV_REUSE_DESCRIPTORS) {
+        check.at[0] = new_at;
+        check.want[0] = new_stamp;
+    } else {
+        if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
+                                           plan->new_live_blocks, ws, flag, L.scan_new, L.desc_new, true, stream,
+                                           L.bucket_new, nullptr, 0))
+            return st;
+        if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new,
+                                             L.bucket_new, L.sorted_new, new_at, new_stamp, stream))
+            return st;
+    }
+    if (dst->layout != kLayoutNHD)
+        return launch_tiles<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size,
+                                   row_stride * sh.new_block_size, dst->layout, ws, L.sorted_new, check, stream);
+    std::vector<std::vector<const HostSlice*>> groups;
+    if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), kUnpackRowsMinShareBytes,
+                                        kUnpackRowsMaxShareBytes, groups))
+        return launch_rows<false>(*plan, groups, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
+                           static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
+    return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
+                              static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
+}
+
 }  // namespace remp
 
 using namespace remp;
@@ -795,13 +854,14 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
     const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
     uint64_t* old_at = reinterpret_cast<uint64_t*>(ws + L.stamp_old);
-    StampCheck check = no_check(ws);
+    int32_t* flag = reinterpret_cast<int32_t*>(ws);
+    StampCheck check = no_check(flag);
     if (flags & REMP_KV_REUSE_DESCRIPTORS) {
         check.at[0] = old_at;
         check.want[0] = old_stamp(*plan);
     } else if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz,
-                                              plan->old_num_blocks, plan->old_live_blocks, ws, L.scan_old, L.desc_old,
-                                              true, stream, -1, old_at, old_stamp(*plan))) {
+                                              plan->old_num_blocks, plan->old_live_blocks, ws, flag, L.scan_old,
+                                              L.desc_old, true, stream, -1, old_at, old_stamp(*plan))) {
         return st;
     }
     if (hnd_single_heads(src->layout, slices))
@@ -828,55 +888,11 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
                            uint32_t flags, hipStream_t stream) {
     clear_error();
     if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
-    if (flags & ~static_cast<uint32_t>(REMP_KV_SKIP_LOCAL | REMP_KV_REUSE_DESCRIPTORS))
-        return fail(REMP_E_INVALID, "unknown flags");
-    if (new_rank < 0 || new_rank >= plan->own_new.world())
-        return fail(REMP_E_RANGE, "new_rank " + std::to_string(new_rank) + " outside [0, " +
-                                      std::to_string(plan->own_new.world()) + ")");
-    if (remp_status st = check_window(plan, layer_begin, layer_end)) return st;
-    if (remp_status st = check_pool(plan, dst, plan->own_new.layers_of_rank(new_rank), plan->shape.new_block_size,
-                                    "destination"))
-        return st;
-    if (!staging) return fail(REMP_E_INVALID, "staging array is NULL");
+    if (remp_status st = check_unpack_args(plan, new_rank, layer_begin, layer_end, staging, dst, flags)) return st;
     if (remp_status st = check_workspace(plan, workspace, workspace_bytes_)) return st;
-    int64_t nnz = 0;
-    uint64_t new_stamp = 0;
-    if (remp_status st = check_new_tables(plan, new_tables, dst, &nnz, &new_stamp)) return st;
-    if (remp_status st = check_dev_tables(plan, new_dev_tables, nnz, "new")) return st;
-
-    std::vector<HostSlice> slices;
-    if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging,
-                                        (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
-        return st;
-    if (layer_begin == layer_end || plan->new_live_blocks == 0) return REMP_OK;   // as in pack
-    const remp_kv_shape& sh = plan->shape;
-    const int64_t row_stride = static_cast<int64_t>(plan->own_new.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
-    const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);
-    uint64_t* new_at = reinterpret_cast<uint64_t*>(ws + L.stamp_new);
-    StampCheck check = no_check(ws);
-    if (flags & REMP_KV_REUSE_DESCRIPTORS) {
-        check.at[0] = new_at;
-        check.want[0] = new_stamp;
-    } else {
-        if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
-                                           plan->new_live_blocks, ws, L.scan_new, L.desc_new, true, stream,
-                                           L.bucket_new, nullptr, 0))
-            return st;
-        if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new,
-                                             L.bucket_new, L.sorted_new, new_at, new_stamp, stream))
-            return st;
-    }
-    if (dst->layout != kLayoutNHD)
-        return launch_tiles<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size,
-                                   row_stride * sh.new_block_size, dst->layout, ws, L.sorted_new, check, stream);
-    std::vector<std::vector<const HostSlice*>> groups;
-    if (kMergeRows && merged_rows_apply(slices, plan->own_new.heads_per_rank(), kUnpackRowsMinShareBytes,
-                                        kUnpackRowsMaxShareBytes, groups))
-        return launch_rows<false>(*plan, groups, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
-                           static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
-    return launch_copy<false>(*plan, slices, plan->new_live_blocks, sh.new_block_size, row_stride * sh.new_block_size,
-                              static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
+    return unpack_impl(plan, new_rank, layer_begin, layer_end, staging, dst, new_tables, new_dev_tables, ws,
+                       reinterpret_cast<int32_t*>(ws), flags, stream);
 }
 
 remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t layer_begin, int32_t layer_end,
@@ -943,7 +959,8 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
     char* ws = static_cast<char*>(workspace);
     uint64_t* old_at = reinterpret_cast<uint64_t*>(ws + L.stamp_old);
     uint64_t* new_at = reinterpret_cast<uint64_t*>(ws + L.stamp_new);
-    StampCheck check = no_check(ws);
+    int32_t* flag = reinterpret_cast<int32_t*>(ws);
+    StampCheck check = no_check(flag);
     if (flags & REMP_KV_REUSE_DESCRIPTORS) {
         check.at[0] = old_at;
         check.want[0] = old_stamp(*plan);
@@ -951,11 +968,11 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
         check.want[1] = new_stamp;
     } else {
         if (remp_status st = launch_expand(*plan, *old_tables, sh.old_block_size, plan->old_nnz,
-                                           plan->old_num_blocks, plan->old_live_blocks, ws, L.scan_old, L.desc_old,
-                                           true, stream, -1, old_at, old_stamp(*plan)))
+                                           plan->old_num_blocks, plan->old_live_blocks, ws, flag, L.scan_old,
+                                           L.desc_old, true, stream, -1, old_at, old_stamp(*plan)))
             return st;
         if (remp_status st = launch_expand(*plan, *new_dev_tables, sh.new_block_size, nnz, new_tables->num_blocks,
-                                           plan->new_live_blocks, ws, L.scan_new, L.desc_new, false, stream,
+                                           plan->new_live_blocks, ws, flag, L.scan_new, L.desc_new, false, stream,
                                            L.bucket_new, nullptr, 0))
             return st;
         if (remp_status st = launch_sort_new(plan->new_live_blocks, new_tables->num_blocks, ws, L.desc_new,

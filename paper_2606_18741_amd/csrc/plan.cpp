@@ -8,6 +8,7 @@
 // the new rank as a receive.  The plan carries no device memory.
 #include <algorithm>
 #include <atomic>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <new>
@@ -114,6 +115,10 @@ remp_status remp_kv_plan(const remp_topo* old_topo, const remp_topo* new_topo, c
     if (!p) return fail(REMP_E_INVALID, "out of host memory");
     static std::atomic<uint64_t> next_serial{1};
     p->serial = next_serial.fetch_add(1);
+    if (const char* wg = std::getenv("REMP_KV_WG_BYTES")) {   // tuning hook, see remp_kv.h
+        const long long v = std::atoll(wg);
+        p->wg_bytes = v > 0 ? std::min<long long>(v, int64_t(1) << 30) : 0;
+    }
     p->old_topo = *old_topo;
     p->new_topo = *new_topo;
     p->shape = s;

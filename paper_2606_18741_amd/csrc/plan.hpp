@@ -76,6 +76,7 @@ struct remp_kv_plan_s {
     std::vector<remp::Pair> pairs;     // ordered by (src, dst)
     std::vector<int32_t> pair_index;   // [old_world * new_world] -> pair or -1
     uint64_t serial = 0;               // unique per plan in the process (descriptor stamps)
+    int64_t wg_bytes = 0;              // tuning hook REMP_KV_WG_BYTES, read once at plan creation (0: built-in)
 };
 
 namespace remp {

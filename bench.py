@@ -23,6 +23,7 @@ import os
 import statistics
 import sys
 import time
+import types
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -57,6 +58,9 @@ def parse():
                          "DeepSeek-R1-Distill-Qwen-32B; 0: skip the weight-shard measurement)")
     ap.add_argument("--prewarm-gib", type=float, default=200.0,
                     help="GiB of device memory written and released before the workload is allocated (0: none)")
+    ap.add_argument("--no-first-touch", action="store_true",
+                    help="skip the first-touch measurement (the same steps timed on a workload allocated before "
+                         "the prewarm, reported as value_first_touch)")
     ap.add_argument("--seed", type=int, default=None, help="override the workload's seed")
     ap.add_argument("--sigma", type=float, default=None,
                     help="override the lognormal sigma of the workload's sequence lengths")
@@ -228,18 +232,6 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     dev = "cuda:0"
-    if args.prewarm_gib > 0:
-        # First use of device memory that no process has used since the machine started is measurably
-        # slower for the scattered unpack writes (MI355X: 5.58-5.66 TB/s in a machine's first benchmark
-        # process against 5.76-5.84 TB/s in later ones); a serving engine's KV pool is long resident.
-        # Write and release most of the memory once before allocating the workload.
-        free, _ = torch.cuda.mem_get_info()
-        n = min(int(args.prewarm_gib * (1 << 30)), int(free * 0.9))
-        scratch = torch.empty(n, dtype=torch.uint8, device=dev)
-        scratch.fill_(0)
-        torch.cuda.synchronize()
-        del scratch
-        torch.cuda.empty_cache()
     w = synthkv.WORKLOADS[args.workload]
     if args.seed is not None:
         w = w.replace(seed=args.seed)
@@ -276,99 +268,139 @@ def main() -> int:
         return range((rank // tp) * per, (rank // tp + 1) * per)
 
     dt = synthkv.torch_dtype_for(w.elem_bytes)
+    nd = synthkv.numpy_dtype_for(w.elem_bytes)
 
     def alloc_layer(tables, tp):
         h_loc = H // tp if tp <= H else 1          # with more tensor ranks than KV heads: one replica each
         return torch.empty((2, tables.num_blocks, tables.block_size, h_loc, D), dtype=dt, device=dev)
 
-    # --- inputs ------------------------------------------------------------
-    t0 = time.time()
-    src_layers = {}
-    for l in layers_of(ro, tpo, ppo):
-        t = alloc_layer(inp.old_tables, tpo)
-        for kv in range(2):
-            synthkv.fill_pool_layer_(t[kv], w.seed, ro, l, kv)
-        src_layers[l] = t
-    # the same bytes serve any layout: the migration is a permutation of them
-    src_arg = tio.pool_arg([src_layers[l] for l in layers_of(ro, tpo, ppo)], inp.old_tables.num_blocks, layout)
-    dst_layers = {l: alloc_layer(inp.new_tables, tpn) for l in layers_of(qn, tpn, ppn)}
-    dst_arg = tio.pool_arg([dst_layers[l] for l in layers_of(qn, tpn, ppn)], inp.new_tables.num_blocks, layout)
-    dto = tio.DeviceTables(rk.HostTables.of(inp.old_tables), dev)
-    dtn = tio.DeviceTables(rk.HostTables.of(inp.new_tables), dev)
-    staging = tio.alloc_staging(plan, sorted(set(pairs_out) | set(pairs_in)), dev)
-    ws = tio.workspace(plan, dev)
-    stream = tio.current_stream()
-    torch.cuda.synchronize()
-    log(f"source and destination pools ready ({time.time() - t0:.1f}s)")
-
-    # staging that other old ranks send to new rank qn: pack them once, untimed
-    foreign_host = {}
     keep_layers = set()
     if not args.no_cpu_baseline:
         per_new = L // ppn
         k = max(1, min(args.cpu_sample_layers, per_new))
         keep_layers = {s * per_new + i for s in range(ppn) for i in range(k)}
-    # Each foreign source packs its whole share (all its destinations, like the
-    # timed pack of old rank ro), so every pack launch in a profile has one shape.
-    for (r, q) in pairs_in:
-        if r == ro:
-            continue
-        tmp = {}
-        for l in layers_of(r, tpo, ppo):
+
+    def build(keep_host: bool):
+        """Allocate and fill the share: old rank ro's pools, new rank qn's pools, every staging buffer ro
+        fills or qn reads, the workspace; the staging other old ranks send to qn is packed once, untimed
+        (each foreign source packs its whole share, so every pack launch in a profile has one shape).
+        keep_host: keep host copies of the foreign sources' sampled layers for the oracle."""
+        t0 = time.time()
+        sh = types.SimpleNamespace()
+        sh.src_layers = {}
+        for l in layers_of(ro, tpo, ppo):
             t = alloc_layer(inp.old_tables, tpo)
             for kv in range(2):
-                synthkv.fill_pool_layer_(t[kv], w.seed, r, l, kv)
-            tmp[l] = t
-            if l in keep_layers and pair_info[(r, q)].layer_begin <= l < pair_info[(r, q)].layer_end:
-                foreign_host[(r, l)] = t.cpu().numpy().view(synthkv.numpy_dtype_for(w.elem_bytes))
-        arg = tio.pool_arg([tmp[l] for l in layers_of(r, tpo, ppo)], inp.old_tables.num_blocks, layout)
-        extra = tio.alloc_staging(plan, [pp for pp in pair_info if pp[0] == r and pp != (r, q)], dev)
-        bufs = dict(extra)
-        bufs[(r, q)] = staging[(r, q)]
-        plan.pack(r, arg, dto.dev, tio.staging_args(bufs, r, W_new, as_src=True), ws, ws.numel(), stream)
+                synthkv.fill_pool_layer_(t[kv], w.seed, ro, l, kv)
+            sh.src_layers[l] = t
+        # the same bytes serve any layout: the migration is a permutation of them
+        sh.src_arg = tio.pool_arg([sh.src_layers[l] for l in layers_of(ro, tpo, ppo)], inp.old_tables.num_blocks,
+                                  layout)
+        sh.dst_layers = {l: alloc_layer(inp.new_tables, tpn) for l in layers_of(qn, tpn, ppn)}
+        sh.dst_arg = tio.pool_arg([sh.dst_layers[l] for l in layers_of(qn, tpn, ppn)], inp.new_tables.num_blocks,
+                                  layout)
+        sh.dto = tio.DeviceTables(rk.HostTables.of(inp.old_tables), dev)
+        sh.dtn = tio.DeviceTables(rk.HostTables.of(inp.new_tables), dev)
+        sh.staging = tio.alloc_staging(plan, sorted(set(pairs_out) | set(pairs_in)), dev)
+        sh.ws = tio.workspace(plan, dev)
+        sh.stream = tio.current_stream()
         torch.cuda.synchronize()
-        if tio.workspace_flag(ws) != 0:
-            raise RuntimeError("device tables disagree with host tables")
-        del tmp, arg, extra, bufs
-        torch.cuda.empty_cache()
-    log(f"foreign staging packed ({time.time() - t0:.1f}s)")
+        sh.foreign_host = {}
+        for (r, q) in pairs_in:
+            if r == ro:
+                continue
+            tmp = {}
+            for l in layers_of(r, tpo, ppo):
+                t = alloc_layer(inp.old_tables, tpo)
+                for kv in range(2):
+                    synthkv.fill_pool_layer_(t[kv], w.seed, r, l, kv)
+                tmp[l] = t
+                if keep_host and l in keep_layers and pair_info[(r, q)].layer_begin <= l < pair_info[(r, q)].layer_end:
+                    sh.foreign_host[(r, l)] = t.cpu().numpy().view(nd)
+            arg = tio.pool_arg([tmp[l] for l in layers_of(r, tpo, ppo)], inp.old_tables.num_blocks, layout)
+            extra = tio.alloc_staging(plan, [pp for pp in pair_info if pp[0] == r and pp != (r, q)], dev)
+            bufs = dict(extra)
+            bufs[(r, q)] = sh.staging[(r, q)]
+            plan.pack(r, arg, sh.dto.dev, tio.staging_args(bufs, r, W_new, as_src=True), sh.ws, sh.ws.numel(),
+                      sh.stream)
+            torch.cuda.synchronize()
+            if tio.workspace_flag(sh.ws) != 0:
+                raise RuntimeError("device tables disagree with host tables")
+            del tmp, arg, extra, bufs
+            torch.cuda.empty_cache()
+        sh.st_out = tio.staging_args(sh.staging, ro, W_new, as_src=True)
+        sh.st_in = tio.staging_args(sh.staging, qn, W_old, as_src=False)
+        log(f"share built: pools, staging and foreign staging ready ({time.time() - t0:.1f}s)")
+        return sh
 
-    st_out = tio.staging_args(staging, ro, W_new, as_src=True)
-    st_in = tio.staging_args(staging, qn, W_old, as_src=False)
-
-    def step(ev=None):
+    def step(sh, ev=None):
         if ev is not None:
             rk.remp_kv_set_trace_events(ev[0].cuda_event, ev[1].cuda_event)
-        plan.pack(ro, src_arg, dto.dev, st_out, ws, ws.numel(), stream)
+        plan.pack(ro, sh.src_arg, sh.dto.dev, sh.st_out, sh.ws, sh.ws.numel(), sh.stream)
         if ev is not None:
             rk.remp_kv_set_trace_events(ev[2].cuda_event, ev[3].cuda_event)
-        plan.unpack(qn, st_in, dst_arg, dtn.host, dtn.dev, ws, ws.numel(), stream)
+        plan.unpack(qn, sh.st_in, sh.dst_arg, sh.dtn.host, sh.dtn.dev, sh.ws, sh.ws.numel(), sh.stream)
         if ev is not None:
             rk.remp_kv_set_trace_events(None, None)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    if tio.workspace_flag(ws) != 0:
-        raise RuntimeError("device tables disagree with host tables")
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    for e4 in evs:           # torch creates the HIP event on first record; the library re-records it
-        for e in e4:
-            e.record()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for i in range(args.steps):
-        step(evs[i])
-    stop.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    ms_per_step = total_ms / max(args.steps, 1)
-    pack_ms = [e[0].elapsed_time(e[1]) for e in evs]
-    unpack_ms = [e[2].elapsed_time(e[3]) for e in evs]
+    def timed(sh):
+        """args.warmup untimed steps, then args.steps steps between two events, with per-call events."""
+        for _ in range(args.warmup):
+            step(sh)
+        torch.cuda.synchronize()
+        if tio.workspace_flag(sh.ws) != 0:
+            raise RuntimeError("device tables disagree with host tables")
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        for e4 in evs:           # torch creates the HIP event on first record; the library re-records it
+            for e in e4:
+                e.record()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(args.steps):
+            step(sh, evs[i])
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / max(args.steps, 1)
+        return ms, [e[0].elapsed_time(e[1]) for e in evs], [e[2].elapsed_time(e[3]) for e in evs]
+
+    first_touch = None
+    if not args.no_first_touch:
+        # the same steps on a share allocated before any prewarm of device memory
+        sh = build(keep_host=False)
+        ft_ms, _, _ = timed(sh)
+        first_touch = {"value": round(traffic / (ft_ms / 1e3) / 1e9, 1), "ms_per_step": round(ft_ms, 4)}
+        log(f"first touch: {ft_ms:.3f} ms/step, {first_touch['value']} GB/s")
+        del sh
+        torch.cuda.empty_cache()
+    if args.prewarm_gib > 0:
+        # First use of device memory that no process has used since the machine started is measurably
+        # slower for the scattered unpack writes (MI355X: 5.58-5.66 TB/s in a machine's first benchmark
+        # process against 5.76-5.84 TB/s in later ones); a serving engine's KV pool is long resident.
+        # Write and release most of the memory once before allocating the workload.
+        free, _ = torch.cuda.mem_get_info()
+        n = min(int(args.prewarm_gib * (1 << 30)), int(free * 0.9))
+        scratch = torch.empty(n, dtype=torch.uint8, device=dev)
+        scratch.fill_(0)
+        torch.cuda.synchronize()
+        del scratch
+        torch.cuda.empty_cache()
+    sh = build(keep_host=not args.no_cpu_baseline)
+    src_layers, dst_layers, staging, ws, stream = sh.src_layers, sh.dst_layers, sh.staging, sh.ws, sh.stream
+    src_arg, dst_arg, dto, dtn = sh.src_arg, sh.dst_arg, sh.dto, sh.dtn
+    ms_per_step, pack_ms, unpack_ms = timed(sh)
     value = traffic / (ms_per_step / 1e3) / 1e9
     log(f"{args.steps} steps: {ms_per_step:.3f} ms/step, pack kernel {statistics.mean(pack_ms):.3f} ms, "
         f"unpack kernel {statistics.mean(unpack_ms):.3f} ms, {value:.1f} GB/s")
+    # what the timed steps wrote in the oracle's sample layers, copied out before anything else runs
+    sample = sorted(keep_layers)
+    got_dst, got_stage = {}, {}
+    if sample:
+        got_dst = {l: dst_layers[l].cpu() for l in sample if l in dst_layers}
+        for key in sorted(set(pairs_out) | set(pairs_in)):
+            _, offs = plan.query(*key)
+            got_stage[key] = {l: staging[key][int(offs[l]):int(offs[l + 1])].cpu() for l in sample
+                              if pair_info[key].layer_begin <= l < pair_info[key].layer_end}
 
     # --- the same share with the local fast path (slices old rank ro keeps as new
     # rank qn go pool to pool; the rest through staging), timed the same way
@@ -441,7 +473,7 @@ def main() -> int:
     weights = None
     spec = WEIGHT_MODELS.get(w.name)
     if args.weight_layers > 0 and spec is not None:
-        weights = bench_weights(args, rk, synthkv, torch, qn, w.new_topo, step, ms_per_step, dev,
+        weights = bench_weights(args, rk, synthkv, torch, qn, w.new_topo, lambda: step(sh), ms_per_step, dev,
                                 getattr(synthkv, spec))
 
     pack_avg, unpack_avg = statistics.mean(pack_ms), statistics.mean(unpack_ms)
@@ -467,21 +499,23 @@ def main() -> int:
         "launches_per_call": prof["launches_per_call"] if prof else None,
     }
 
-    # --- CPU baseline: the oracle on a bounded sample of the same workload ----
+    # --- CPU baseline: the oracle on a bounded sample of the same workload, and the timed output checked
+    # against it ----
     cpu = None
+    parity = None
     if not args.no_cpu_baseline:
         import oracle
-        nd = synthkv.numpy_dtype_for(w.elem_bytes)
-        sample = sorted(keep_layers)
         old_h = {ro: {l: src_layers[l].cpu().numpy().view(nd) for l in sample if l in src_layers}}
-        for (r, l), a in foreign_host.items():
+        for (r, l), a in sh.foreign_host.items():
             old_h.setdefault(r, {})[l] = a
-        new_h = {qn: {l: np.empty(tuple(dst_layers[l].shape), dtype=nd) for l in sample if l in dst_layers}}
+        # pre-filled with what the GPU left there, so the comparison below checks the rows the oracle writes
+        # (every live row of the sample layers); dead rows are compared by the test suite
+        new_h = {qn: {l: got_dst[l].numpy().view(nd).copy() for l in got_dst}}
         want = sorted(set(pairs_out) | set(pairs_in))
         log(f"oracle on layers {sample} ...")
         t1 = time.perf_counter()
-        oracle.reshard(old_h, new_h, oracle.Topology(tpo, ppo), oracle.Topology(tpn, ppn), L, H,
-                       inp.old_tables, inp.new_tables, layers=sample, pairs=want)
+        ref = oracle.reshard(old_h, new_h, oracle.Topology(tpo, ppo), oracle.Topology(tpn, ppn), L, H,
+                             inp.old_tables, inp.new_tables, layers=sample, pairs=want)
         cpu_s = time.perf_counter() - t1
         moved = 0
         for key in want:
@@ -508,6 +542,26 @@ def main() -> int:
         cpu["parallel"] = {"value": round(moved / par_s / 1e9, 3), "unit": "GB/s", "cores": threads,
                            "seconds": round(par_s, 2), "how": "one layer per task, ThreadPoolExecutor"}
         log(f"oracle on {threads} threads: {par_s:.1f}s, {moved / par_s / 1e9:.2f} GB/s")
+
+        bad, checked = [], 0
+        for key, per_layer in got_stage.items():
+            for l, g in per_layer.items():
+                e = np.ascontiguousarray(ref[key][l]).reshape(-1).view(np.uint8)
+                if not torch.equal(g, torch.from_numpy(e)):
+                    bad.append(f"staging {key} layer {l}")
+                checked += g.numel()
+        for l, g in got_dst.items():
+            e = new_h[qn][l]
+            if not torch.equal(g.view(-1).view(torch.uint8),
+                               torch.from_numpy(np.ascontiguousarray(e).reshape(-1).view(np.uint8))):
+                bad.append(f"new pool layer {l}")
+            checked += g.numel() * g.element_size()
+        parity = {"ok": not bad, "against": "oracle", "layers": sample, "compared_bytes": checked,
+                  "mismatches": bad[:20],
+                  "what": f"every staging byte of the pairs old rank {ro} fills and new rank {qn} reads, and every "
+                          f"live row of new rank {qn}'s pool, in the sample layers, as the timed steps left them"}
+        log(f"parity against the oracle: {'ok' if not bad else 'MISMATCH ' + ', '.join(bad[:5])} "
+            f"({checked / 1e9:.2f} GB compared)")
 
     out = {
         "metric": "KV migration GB/s (pack+unpack) and % of MI355X HBM peak, 70B GQA share",
@@ -536,6 +590,9 @@ def main() -> int:
             "pack_kernel_ms": round(pack_avg, 4),
             "unpack_kernel_ms": round(unpack_avg, 4),
         },
+        "parity": parity,
+        "value_first_touch": first_touch["value"] if first_touch else None,
+        "first_touch": first_touch,
         "roofline": roofline,
         "local_fast_path": local,
         "layer_streaming": streaming,
@@ -543,6 +600,9 @@ def main() -> int:
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+    if parity is not None and not parity["ok"]:
+        print("bench.py: the timed output differs from the oracle", file=sys.stderr)
+        return 1
     return 0
 
 

@@ -44,6 +44,9 @@ static thread_local hipEvent_t g_trace_stop = nullptr;
 // tuning override (REMP_KV_WG_BYTES when the plan was created).
 static int64_t wg_target(const remp_kv_plan_t& p, int64_t builtin) { return p.wg_bytes > 0 ? p.wg_bytes : builtin; }
 
+// Bound on a copy workgroup's flattened (unit, row, vector) index space.
+constexpr uint64_t kMaxWgVectors = uint64_t(1) << 31;
+
 struct HostSlice {
     uint64_t paged_k, paged_v, stage;
     uint32_t row_bytes;
@@ -171,10 +174,11 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     const bool small = per_unit <= kSmallUnitBytes;
     const int64_t target = wg_target(p, small ? kSmallWgBytes : kLargeWgBytes);
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
-    // the flattened per-workgroup index must stay below 2^32
-    while (C > 1 && static_cast<uint64_t>(C) * bs * (max_row / vec) >= (uint64_t(1) << 32)) C >>= 1;
-    if (static_cast<uint64_t>(bs) * (max_row / vec) >= (uint64_t(1) << 32))
-        return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^32 vectors");
+    // the flattened per-workgroup index stays below 2^31, so a lane's index plus the loop stride
+    // (at most 1024 threads x 4 vectors) never wraps in 32 bits
+    while (C > 1 && static_cast<uint64_t>(C) * bs * (max_row / vec) >= kMaxWgVectors) C >>= 1;
+    if (static_cast<uint64_t>(bs) * (max_row / vec) >= kMaxWgVectors)
+        return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^31 vectors");
 
     CopyArgs a;
     std::memset(&a, 0, sizeof(a));
@@ -352,9 +356,9 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
     const bool small = per_unit <= kSmallUnitBytes;
     const int64_t target = wg_target(p, small ? kSmallWgBytes : kLargeWgBytes);
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
-    while (C > 1 && static_cast<uint64_t>(C) * bs * (row_stride / vec) >= (uint64_t(1) << 32)) C >>= 1;
-    if (static_cast<uint64_t>(bs) * (row_stride / vec) >= (uint64_t(1) << 32))
-        return fail(REMP_E_UNSUPPORTED, "a block of one row exceeds 2^32 vectors");
+    while (C > 1 && static_cast<uint64_t>(C) * bs * (row_stride / vec) >= kMaxWgVectors) C >>= 1;
+    if (static_cast<uint64_t>(bs) * (row_stride / vec) >= kMaxWgVectors)
+        return fail(REMP_E_UNSUPPORTED, "a block of one row exceeds 2^31 vectors");
     MergeArgs a;
     std::memset(&a, 0, sizeof(a));
     a.desc = reinterpret_cast<const BlockDesc*>(ws + desc_off);
@@ -690,8 +694,9 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     int32_t C = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kMaxUnitsPerWg, target / per_unit)));
     C = std::min<int32_t>(C, std::max<int32_t>(1, kMaxLocalRows / bn));
     if (bn > kMaxLocalRows) return fail(REMP_E_UNSUPPORTED, "new block size above the local-copy row limit");
-    if (static_cast<uint64_t>(C) * bn * (max_row / vec) >= (uint64_t(1) << 32))
-        return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^32 vectors");
+    while (C > 1 && static_cast<uint64_t>(C) * bn * (max_row / vec) >= kMaxWgVectors) C >>= 1;
+    if (static_cast<uint64_t>(bn) * (max_row / vec) >= kMaxWgVectors)
+        return fail(REMP_E_UNSUPPORTED, "a block of one slice exceeds 2^31 vectors");
 
     LocalArgs a;
     std::memset(&a, 0, sizeof(a));

@@ -1,22 +1,22 @@
 """GPU parity at the workloads' full sizes, in the launch configuration the benchmark times.
 
-The GPU plays old rank r0 (packs everything it sends) and new rank q0 (unpacks
-everything it receives); the staging other old ranks send to q0 is packed by
-the same library from their own generated pools.  Large workloads run in layer
-windows (the paper's layer-wise streaming) to bound memory, expanding the
-block tables in the first pack and unpack only and reusing the descriptors in
-every later call; the 70B GQA share runs as one window, exactly like the
-benchmark.
+The GPU plays old rank r0 (one pack call for everything it sends) and new rank
+q0 (one unpack call for everything it receives); the staging other old ranks
+send to q0 is packed first by the same library from their own generated pools.
+This is exactly the benchmark's step.
 
-Checked against the oracle:
-* sampled staging rows and sampled new-pool rows (uniform over tokens, plus the
-  first and last token of every sequence), whose expected bytes the oracle's
-  point queries locate in the generated source pools;
-* properties over every byte: the new pool differs from its sentinel pre-fill
-  at exactly the live (block, slot) rows of the new tables, and the source
-  pools are unchanged.
+Checked against the oracle, after a quick pre-check of sampled rows located by
+the oracle's point queries:
+* every staging byte of every pair r0 sends or q0 receives, and every byte of
+  q0's new pool (live rows and the sentinel rows the unpack must not touch),
+  equal oracle.reshard run on the same generated inputs, layer window by layer
+  window (the windows only bound host memory; the GPU ran one call per phase);
+* every byte of r0's source pool is unchanged.
+The 70B GQA share also runs with HND and ROCm pools (sampled rows).
 """
 from __future__ import annotations
+
+import os
 
 import numpy as np
 import pytest
@@ -28,19 +28,12 @@ from paper_2606_18741_amd import torch_io as tio
 import synthkv
 
 from gpu_harness import DeviceTables, RankPool, log, shape_of
-from hostpools import element_offsets, local_heads
+from hostpools import element_offsets, local_heads, source_stream_rank
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 T = oracle.Topology
-FULL = {
-    "mha7b": None,          # one window
-    "mha13b": 20,           # layers per window
-    "gqa70b": None,
-    "gqa70b_long": 20,
-    "qwen30b": None,
-    "ds32b": 16,
-}
+FULL = ["mha7b", "mha13b", "gqa70b", "gqa70b_long", "qwen30b", "ds32b"]
 
 
 def _sample_tokens(rng, lens, n):
@@ -171,25 +164,6 @@ def _check_new_pool_layout(w, inp, qn, dst, l0, l1, rng, layout, src_layout, nsa
     return n
 
 
-def _live_mask(tables):
-    m = np.zeros((tables.num_blocks, tables.block_size), dtype=bool)
-    for s in range(tables.num_seqs):
-        blk, slot = oracle.token_slots(tables, s)
-        m[blk, slot] = True
-    return m
-
-
-def _check_live_rows_exactly(w, dst, qn, mask_dev):
-    """Every byte of the new pool: differs from the sentinel exactly at live rows."""
-    for l, store in dst.store.items():
-        ref = torch.empty_like(store)
-        for kv in range(2):
-            synthkv.fill_sentinel_(ref[kv], w.seed, 0, qn, l, kv)
-            changed = (ref[kv] != store[kv]).flatten(2).any(-1)          # [nb, bs]
-            assert torch.equal(changed, mask_dev), f"layer {l} kv {kv}: written rows != live rows"
-        del ref
-
-
 def _check_sources_unchanged(w, src, r):
     for l, store in src.store.items():
         ref = torch.empty_like(store)
@@ -199,73 +173,136 @@ def _check_sources_unchanged(w, src, r):
         del ref
 
 
-@pytest.mark.timeout(600)
+def _pool_layer(w, topo, tables, rank, l, fill):
+    """One generated [2, nb, bs, H_loc, D] layer of a rank, on the GPU (same bytes as RankPool)."""
+    tp = topo[0]
+    t = torch.empty((2, tables.num_blocks, tables.block_size, local_heads(w.num_kv_heads, tp), w.head_dim),
+                    dtype=synthkv.torch_dtype_for(w.elem_bytes), device="cuda")
+    for kv in range(2):
+        if fill == "source":
+            synthkv.fill_pool_layer_(t[kv], w.seed, source_stream_rank(rank, tp, w.num_kv_heads), l, kv)
+        else:
+            synthkv.fill_sentinel_(t[kv], w.seed, 0, rank, l, kv)
+    return t
+
+
+def _host(t: torch.Tensor, elem_bytes: int) -> np.ndarray:
+    return t.cpu().numpy().view(synthkv.numpy_dtype_for(elem_bytes))
+
+
+def _equal(got: torch.Tensor, want: np.ndarray) -> bool:
+    """Every byte of a device buffer against a host array (compared on the host, all cores)."""
+    g = got.cpu().reshape(-1).view(torch.uint8)
+    return torch.equal(g, torch.from_numpy(np.ascontiguousarray(want).reshape(-1).view(np.uint8)))
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", list(FULL))
-def test_full_size_sampled(name):
+def test_full_size_every_byte(name):
+    """One rank's share at full size, launched as the benchmark launches it (one pack call of old rank r0 for
+    all its destinations, one unpack call of new rank q0 from all its sources, after the other sources of q0
+    packed their shares), then compared with the oracle byte for byte: every staging byte of every pair r0
+    sends or q0 receives, every byte of q0's new pool (live rows and untouched sentinel rows), and every byte
+    of r0's source pool (unchanged).  Sampled rows are checked first as a quick pre-check."""
+    import concurrent.futures
+    torch.cuda.empty_cache()
     w = synthkv.WORKLOADS[name]
     inp = synthkv.make_inputs(w)
-    L = w.num_layers
+    L, H, e = w.num_layers, w.num_kv_heads, w.elem_bytes
     ro, qn = w.role
+    old_t, new_t = T(*w.old_topo), T(*w.new_topo)
     plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
     W_old, W_new = plan.info.old_world, plan.info.new_world
     pairs_out = [(p.src, p.dst) for p in plan.pairs if p.src == ro]
     pairs_in = [(p.src, p.dst) for p in plan.pairs if p.dst == qn]
+    pairs = sorted(set(pairs_out) | set(pairs_in))
     pinfo = {(p.src, p.dst): p for p in plan.pairs}
-    step = FULL[name] or L
-    windows = [(a, min(L, a + step)) for a in range(0, L, step)]
     dto, dtn = DeviceTables(inp.old_tables), DeviceTables(inp.new_tables)
     ws = tio.workspace(plan, "cuda")
     stream = tio.current_stream()
-    mask_dev = torch.from_numpy(_live_mask(inp.new_tables)).cuda()
-    rng = np.random.default_rng(2024)
-    checked = 0
-    # windowed runs stream as a serving engine would: only the first pack and the first unpack expand
-    # the block tables, every later call reuses their descriptors
-    reuse = rk.REMP_KV_REUSE_DESCRIPTORS
-    old_expanded = new_expanded = False
-    for (l0, l1) in windows:
-        log(f"[fullsize] {name} window [{l0}, {l1}) T={plan.info.total_tokens}")
-        win = range(l0, l1)
-        src = RankPool(w, w.old_topo, inp.old_tables, ro, "source", layers=win)
-        dst = RankPool(w, w.new_topo, inp.new_tables, qn, "sentinel", layers=win)
-        staging = tio.alloc_staging(plan, sorted(set(pairs_out) | set(pairs_in)), "cuda", window=(l0, l1))
-        for (r, q) in pairs_in:
-            p = pinfo[(r, q)]
-            if r == ro or p.layer_end <= l0 or p.layer_begin >= l1:
-                continue
-            fp = RankPool(w, w.old_topo, inp.old_tables, r, "source", layers=win)
-            extra = tio.alloc_staging(plan, [k for k in pinfo if k[0] == r and k != (r, q)], "cuda",
-                                      window=(l0, l1))
-            bufs = dict(extra)
-            bufs[(r, q)] = staging[(r, q)]
-            plan.pack(r, fp.arg, dto.dev, tio.staging_args(bufs, r, W_new, True), ws, ws.numel(), stream, l0, l1,
-                      flags=reuse if old_expanded else 0)
-            old_expanded = True
-            torch.cuda.synchronize()
-            assert tio.workspace_flag(ws) == 0
-            del fp, extra, bufs
-        plan.pack(ro, src.arg, dto.dev, tio.staging_args({k: staging[k] for k in pairs_out if k in staging},
-                                                         ro, W_new, True), ws, ws.numel(), stream, l0, l1,
-                  flags=reuse if old_expanded else 0)
-        old_expanded = True
+    log(f"[fullsize] {name}: T={plan.info.total_tokens}, pairs out {pairs_out}, in {pairs_in}")
+    src = RankPool(w, w.old_topo, inp.old_tables, ro, "source")
+    dst = RankPool(w, w.new_topo, inp.new_tables, qn, "sentinel")
+    staging = tio.alloc_staging(plan, pairs, "cuda")
+    for (r, q) in pairs_in:                       # the other sources of q0 pack their whole shares
+        if r == ro:
+            continue
+        fp = RankPool(w, w.old_topo, inp.old_tables, r, "source")
+        extra = tio.alloc_staging(plan, [k for k in pinfo if k[0] == r and k != (r, q)], "cuda")
+        bufs = dict(extra)
+        bufs[(r, q)] = staging[(r, q)]
+        plan.pack(r, fp.arg, dto.dev, tio.staging_args(bufs, r, W_new, True), ws, ws.numel(), stream)
         torch.cuda.synchronize()
         assert tio.workspace_flag(ws) == 0
-        plan.unpack(qn, tio.staging_args({k: staging[k] for k in pairs_in if k in staging}, qn, W_old, False),
-                    dst.arg, dtn.host, dtn.dev, ws, ws.numel(), stream, l0, l1, flags=reuse if new_expanded else 0)
-        new_expanded = True
-        torch.cuda.synchronize()
-        assert tio.workspace_flag(ws) == 0
-        for pair in sorted(set(pairs_out) | set(pairs_in)):
-            if pair in staging:
-                checked += _check_staging(w, plan, inp, pair, staging[pair], l0, l1, rng)
-        if dst.store:
-            checked += _check_new_pool(w, inp, qn, dst, l0, l1, rng)
-            _check_live_rows_exactly(w, dst, qn, mask_dev)
-        _check_sources_unchanged(w, src, ro)
-        log(f"[fullsize] {name} window [{l0}, {l1}) ok, {checked} sampled rows so far")
-        del src, dst, staging
+        del fp, extra, bufs
         torch.cuda.empty_cache()
-    assert checked > 0
+    plan.pack(ro, src.arg, dto.dev, tio.staging_args({k: staging[k] for k in pairs_out}, ro, W_new, True), ws,
+              ws.numel(), stream)
+    plan.unpack(qn, tio.staging_args({k: staging[k] for k in pairs_in}, qn, W_old, False), dst.arg, dtn.host,
+                dtn.dev, ws, ws.numel(), stream)
+    torch.cuda.synchronize()
+    assert tio.workspace_flag(ws) == 0
+    log(f"[fullsize] {name}: migrated")
+
+    rng = np.random.default_rng(2024)             # quick pre-check on sampled rows
+    for pair in pairs:
+        _check_staging(w, plan, inp, pair, staging[pair], 0, L, rng)
+    _check_new_pool(w, inp, qn, dst, 0, L, rng)
+    log(f"[fullsize] {name}: sampled rows ok")
+
+    # every byte, in windows of layers sized to bound host memory
+    layer_bytes = {l: t.numel() * t.element_size() for l, t in dst.store.items()}
+    src_bytes = max(t.numel() * t.element_size() for t in src.store.values())
+    del src.arg, dst.arg                          # layers are freed as soon as they are compared
+    per_layer = 4 * src_bytes + 3 * max(layer_bytes.values(), default=0)
+    span = max(1, min(L, int(48e9 // max(per_layer, 1))))
+    offs = {k: plan.query(*k)[1] for k in pairs}
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    compared = 0
+    with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+        for l0 in range(0, L, span):
+            win = list(range(l0, min(L, l0 + span)))
+            old_h = {ro: {}}
+            for l in win:                         # host copy of the source layer, checked unchanged, then freed
+                if l not in src.store:
+                    continue
+                old_h[ro][l] = _host(src.store[l], e)
+                for kv in range(2):
+                    ref = torch.empty_like(src.store[l][kv])
+                    synthkv.fill_pool_layer_(ref, w.seed, source_stream_rank(ro, w.old_topo[0], H), l, kv)
+                    assert torch.equal(ref, src.store[l][kv]), f"source layer {l} kv {kv} was modified"
+                    del ref
+                del src.store[l]
+            for (r, q) in pairs_in:
+                if r != ro:
+                    lay = [l for l in win if pinfo[(r, q)].layer_begin <= l < pinfo[(r, q)].layer_end]
+                    old_h.setdefault(r, {}).update(
+                        {l: _host(_pool_layer(w, w.old_topo, inp.old_tables, r, l, "source"), e) for l in lay})
+            new_h = {qn: {l: _host(_pool_layer(w, w.new_topo, inp.new_tables, qn, l, "sentinel"), e)
+                          for l in win if l in dst.store}}
+            old_h = {r: d for r, d in old_h.items() if d}
+            if not old_h:                         # no pair of this share carries these layers
+                continue
+            parts = list(ex.map(lambda l: oracle.reshard(old_h, new_h, old_t, new_t, L, H, inp.old_tables,
+                                                         inp.new_tables, layers=[l], pairs=pairs), win))
+            for l, st in zip(win, parts):
+                for pair, items in st.items():
+                    if l not in items:
+                        continue
+                    a, b = int(offs[pair][l]), int(offs[pair][l + 1])
+                    assert _equal(staging[pair][a:b], items[l]), f"staging {pair} layer {l} differs from the oracle"
+                    compared += b - a
+                if l in dst.store:
+                    assert _equal(dst.store[l], new_h[qn][l]), f"new pool layer {l} differs from the oracle"
+                    compared += layer_bytes[l]
+                    del dst.store[l]
+            log(f"[fullsize] {name}: layers [{win[0]}, {win[-1] + 1}) equal the oracle, {compared / 1e9:.1f} GB "
+                f"compared so far")
+            del old_h, new_h, parts
+    want = sum(pinfo[k].staging_bytes for k in pairs) + sum(layer_bytes.values())
+    assert compared == want, (compared, want)
+    del src, dst, staging
+    torch.cuda.empty_cache()
 
 
 LAYOUT_FULL = [(1, 1, False), (2, 2, False), (0, 2, False), (2, 2, True), (1, 0, True)]

@@ -286,6 +286,32 @@ REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank
                            const remp_dev_tables* new_dev_tables,
                            void* workspace, int64_t workspace_bytes, uint32_t flags, hipStream_t stream);
 
+/* Allocation-free unpack, for callers that cannot allocate device memory or
+ * pass a workspace: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid allocation.  Same arguments, validation and result as
+ * remp_kv_unpack, but the workspace areas live in a static device array of the
+ * library (8 MiB, REMP_KV_NOALLOC_SCRATCH_BYTES) instead of a caller buffer:
+ * plans whose remp_kv_workspace_bytes exceeds that size are refused with
+ * REMP_E_SIZE before anything is enqueued.  The call allocates no device
+ * memory and calls no allocating routine; its first call on each device
+ * resolves that device's copy of the array (hipGetSymbolAddress), so make it
+ * outside graph capture; later calls only launch kernels.
+ * status: NULL, or a 4-byte aligned device int32 that receives the status
+ * flag remp_kv_workspace_bytes describes (0, 1 or 2); with NULL the flag stays
+ * in the static array.
+ * Every call on one device shares that device's array and finds the contents
+ * the last call left: REMP_KV_REUSE_DESCRIPTORS reuses the descriptors of the
+ * last expanding call on the device when their stamps match (flag 2
+ * otherwise).  Calls that can overlap on one device (different streams, or
+ * threads) race on the array and must be ordered by the caller. */
+#define REMP_KV_NOALLOC_SCRATCH_BYTES (8 << 20)
+REMP_API remp_status remp_kv_unpack_noalloc(const remp_kv_plan_t* plan, int32_t new_rank,
+                                   int32_t layer_begin, int32_t layer_end,
+                                   const remp_buffer* staging,
+                                   const remp_kv_pool* dst, const remp_block_tables* new_tables,
+                                   const remp_dev_tables* new_dev_tables,
+                                   int32_t* status, uint32_t flags, hipStream_t stream);
+
 /* Local copy (Section 3.4.3: when a slice's source and destination are the
  * same worker it is copied locally instead of transferred): for the slices
  * that `rank` sends to itself (same global rank id in both topologies) in

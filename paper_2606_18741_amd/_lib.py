@@ -23,7 +23,8 @@ STATUS = {0: "REMP_OK", -1: "REMP_E_INVALID", -2: "REMP_E_UNSUPPORTED", -3: "REM
 # every symbol include/remp_kv.h and include/remp_weights.h declare
 EXPORTED = (
     "remp_kv_plan", "remp_kv_plan_destroy", "remp_kv_plan_get_info", "remp_kv_plan_get_pair",
-    "remp_kv_plan_query", "remp_kv_workspace_bytes", "remp_kv_pack", "remp_kv_unpack", "remp_kv_copy_local",
+    "remp_kv_plan_query", "remp_kv_workspace_bytes", "remp_kv_pack", "remp_kv_unpack", "remp_kv_unpack_noalloc",
+    "remp_kv_copy_local",
     "remp_kv_set_trace_events", "remp_status_string", "remp_last_error", "remp_kv_version",
     "remp_w_plan", "remp_w_plan_destroy", "remp_w_shard_shape", "remp_w_shard_bytes", "remp_w_load",
 )
@@ -137,6 +138,10 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
                                    POINTER(BlockTables), POINTER(DevTables), c_void_p, c_int64, ctypes.c_uint32,
                                    c_void_p]
     lib.remp_kv_unpack.restype = st
+    lib.remp_kv_unpack_noalloc.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(Buffer), POINTER(Pool),
+                                           POINTER(BlockTables), POINTER(DevTables), c_void_p, ctypes.c_uint32,
+                                           c_void_p]
+    lib.remp_kv_unpack_noalloc.restype = st
     lib.remp_kv_copy_local.argtypes = [c_void_p, c_int32, c_int32, c_int32, POINTER(Pool), POINTER(DevTables),
                                        POINTER(Pool), POINTER(BlockTables), POINTER(DevTables), c_void_p, c_int64,
                                        ctypes.c_uint32, c_void_p]
@@ -316,6 +321,14 @@ def remp_kv_unpack(plan, new_rank: int, layer_begin: int, layer_end: int, stagin
                                  int(workspace_bytes), int(flags), c_void_p(stream)), "remp_kv_unpack")
 
 
+def remp_kv_unpack_noalloc(plan, new_rank: int, layer_begin: int, layer_end: int, staging, dst: PoolArg,
+                           new_tables: HostTables, new_dev_tables: DevTables, status, flags: int,
+                           stream: int) -> None:
+    _check(load().remp_kv_unpack_noalloc(plan, new_rank, layer_begin, layer_end, staging, _ref(dst),
+                                         _ref(new_tables), _ref(new_dev_tables), _ptr(status), int(flags),
+                                         c_void_p(stream)), "remp_kv_unpack_noalloc")
+
+
 def remp_kv_copy_local(plan, rank: int, layer_begin: int, layer_end: int, src: PoolArg, old_dev_tables: DevTables,
                        dst: PoolArg, new_tables: HostTables, new_dev_tables: DevTables, workspace,
                        workspace_bytes: int, flags: int, stream: int) -> None:
@@ -471,6 +484,12 @@ class Plan:
                flags: int = 0) -> None:
         remp_kv_unpack(self.handle, new_rank, layer_begin, self.num_layers if layer_end is None else layer_end,
                        staging, dst, new_tables, new_dev_tables, workspace, workspace_bytes, flags, stream)
+
+    def unpack_noalloc(self, new_rank, staging, dst: PoolArg, new_tables: HostTables, new_dev_tables: DevTables,
+                       status, stream, layer_begin: int = 0, layer_end: Optional[int] = None,
+                       flags: int = 0) -> None:
+        remp_kv_unpack_noalloc(self.handle, new_rank, layer_begin, self.num_layers if layer_end is None else layer_end,
+                               staging, dst, new_tables, new_dev_tables, status, flags, stream)
 
     def copy_local(self, rank, src: PoolArg, old_dev_tables: DevTables, dst: PoolArg, new_tables: HostTables,
                    new_dev_tables: DevTables, workspace, workspace_bytes, stream, layer_begin: int = 0,

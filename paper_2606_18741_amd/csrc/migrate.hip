@@ -17,8 +17,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <unordered_set>
 #include <vector>
@@ -816,6 +818,45 @@ static remp_status unpack_impl(const remp_kv_plan_t* plan, int32_t new_rank, int
                               static_cast<int32_t>(row_stride), ws, L.sorted_new, check, stream);
 }
 
+// ---------------------------------------------------------------------------
+// static scratch of the allocation-free unpack
+// ---------------------------------------------------------------------------
+//
+// remp_kv_unpack_noalloc keeps its workspace areas in this array instead of a
+// caller buffer.  Each device that loads the library holds its own copy until
+// the process ends; the host-side name below is only a stand-in, so kernels
+// get the device address that hipGetSymbolAddress returns for the current
+// device, resolved once per device on that device's first call.
+constexpr int64_t kScratchBytes = REMP_KV_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+static std::atomic<char*> g_scratch_ptr[kMaxScratchDevices];
+static std::mutex g_scratch_mu;
+
+static remp_status scratch_of_current_device(char** out) {
+    int dev = -1;
+    if (remp_status st = hip_check(hipGetDevice(&dev), "hipGetDevice")) return st;
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(REMP_E_UNSUPPORTED, "device index " + std::to_string(dev) + " beyond the static scratch table");
+    char* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            void* addr = nullptr;
+            if (remp_status st = hip_check(hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)),
+                                           "hipGetSymbolAddress(scratch)"))
+                return st;
+            if (!addr || !aligned(addr, 256)) return fail(REMP_E_HIP, "static scratch has no 256-byte aligned address");
+            p = static_cast<char*>(addr);
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return REMP_OK;
+}
+
 }  // namespace remp
 
 using namespace remp;
@@ -898,6 +939,23 @@ remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank, int32_t
     char* ws = static_cast<char*>(workspace);
     return unpack_impl(plan, new_rank, layer_begin, layer_end, staging, dst, new_tables, new_dev_tables, ws,
                        reinterpret_cast<int32_t*>(ws), flags, stream);
+}
+
+remp_status remp_kv_unpack_noalloc(const remp_kv_plan_t* plan, int32_t new_rank, int32_t layer_begin,
+                                   int32_t layer_end, const remp_buffer* staging, const remp_kv_pool* dst,
+                                   const remp_block_tables* new_tables, const remp_dev_tables* new_dev_tables,
+                                   int32_t* status, uint32_t flags, hipStream_t stream) {
+    clear_error();
+    if (!plan) return fail(REMP_E_INVALID, "plan is NULL");
+    if (workspace_bytes(*plan) > kScratchBytes)
+        return fail(REMP_E_SIZE, "the plan needs " + std::to_string(workspace_bytes(*plan)) +
+                                     " bytes of scratch, the static scratch holds " + std::to_string(kScratchBytes));
+    if (status && !aligned(status, 4)) return fail(REMP_E_ALIGN, "status is not 4-byte aligned");
+    if (remp_status st = check_unpack_args(plan, new_rank, layer_begin, layer_end, staging, dst, flags)) return st;
+    char* ws = nullptr;
+    if (remp_status st = scratch_of_current_device(&ws)) return st;
+    return unpack_impl(plan, new_rank, layer_begin, layer_end, staging, dst, new_tables, new_dev_tables, ws,
+                       status ? status : reinterpret_cast<int32_t*>(ws), flags, stream);
 }
 
 remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t layer_begin, int32_t layer_end,

@@ -136,9 +136,10 @@ WORKLOADS = {w.name: w for w in (TINY, MHA_7B, MHA_13B, GQA_70B, GQA_70B_LONG, Q
 def reduced(w: KVWorkload, num_seqs: int = 5, max_len: int = 300, seed_offset: int = 100) -> KVWorkload:
     """Same shape, topology and pool law as `w`, with a small live population.
 
-    Used where a full-size run would be too slow for the CPU oracle: the layer,
-    head and block structure is unchanged, so a copy still spans many tiles
-    and ends in partial blocks.
+    Used by the many small parity cases (all ranks, edge cases, layouts, the
+    CPU model of the kernels); the full-size populations are compared byte for
+    byte in the full-size GPU tests.  The layer, head and block structure is
+    unchanged, so a copy still spans many tiles and ends in partial blocks.
     """
     return w.replace(
         name=w.name + "_reduced",

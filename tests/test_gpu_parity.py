@@ -25,6 +25,8 @@ from gpu_harness import (DeviceTables, RankPool, Workspace, log, rank_layers, sh
 
 pytestmark = pytest.mark.gpu
 
+from edgecases import EDGE, custom as _custom
+
 T = oracle.Topology
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -176,54 +178,6 @@ def test_layer_windows_match_whole():
 # ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
-
-def _custom(**kw):
-    base = dict(name="edge", num_layers=4, num_kv_heads=8, head_dim=64, elem_bytes=2, dtype="u16",
-                old_block_size=16, new_block_size=16, num_seqs=6, length_law=("uniform", 0, 90),
-                pool_law=("slack", 1.3), old_topo=(2, 1), new_topo=(1, 2), role="all", seed=21)
-    base.update(kw)
-    return synthkv.KVWorkload(**base)
-
-
-EDGE = {
-    "heads_not_nested_reblock": _custom(num_layers=6, num_kv_heads=12, head_dim=32, old_topo=(3, 1),
-                                        new_topo=(2, 3), old_block_size=8, new_block_size=16),
-    "fp8_elements": _custom(elem_bytes=1, old_topo=(4, 1), new_topo=(1, 4)),
-    "fp32_elements": _custom(elem_bytes=4, head_dim=16, old_topo=(1, 2), new_topo=(8, 1)),
-    "odd_row_bytes": _custom(num_kv_heads=4, head_dim=3, old_topo=(2, 1), new_topo=(4, 1)),
-    "identity_2x2": _custom(old_topo=(2, 2), new_topo=(2, 2)),
-    "block_shrink_32_to_8": _custom(old_block_size=32, new_block_size=8, old_topo=(1, 1), new_topo=(2, 2)),
-    "non_power_of_two_block": _custom(old_block_size=12, new_block_size=5, old_topo=(2, 2), new_topo=(4, 1)),
-    "one_token": _custom(num_seqs=1, length_law=("fixed", 1)),
-    "long_single_sequence": _custom(num_seqs=1, length_law=("fixed", 20011), num_layers=2, num_kv_heads=2,
-                                    old_topo=(2, 1), new_topo=(1, 2), head_dim=128),
-    "fragmented_pool": _custom(pool_law=("fragmented", 0.5), num_seqs=12),
-    "all_empty": _custom(length_law=("fixed", 0)),
-    "many_sequences": _custom(num_seqs=1500, length_law=("uniform", 0, 9), num_layers=2),
-    # GQA with more tensor ranks than KV heads (e.g. 4 KV heads at TP8): heads are replicated
-    "replicated_tp8_to_tp2": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(8, 1), new_topo=(2, 1)),
-    "replicated_tp2pp2_to_tp8": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(2, 2),
-                                        new_topo=(8, 1)),
-    "replicated_tp16_to_tp8pp2": _custom(num_layers=8, num_kv_heads=4, head_dim=64, old_topo=(16, 1),
-                                         new_topo=(8, 2), old_block_size=16, new_block_size=32),
-    "replicated_keep_local": _custom(num_layers=8, num_kv_heads=4, head_dim=128, old_topo=(8, 1), new_topo=(4, 2)),
-    # several sources fill each new row with equal shares of >= 256 B: unpack writes whole rows (the fp8 case
-    # below has four 512 B shares; heads_not_nested_reblock has unequal shares and takes per-slice copies)
-    "merged_rows_mha": _custom(num_layers=4, num_kv_heads=16, head_dim=128, old_topo=(4, 1), new_topo=(2, 2)),
-    "merged_rows_reblock": _custom(num_layers=4, num_kv_heads=32, head_dim=128, old_topo=(8, 1),
-                                   new_topo=(2, 2), old_block_size=16, new_block_size=32),
-    # several destinations split an old rank's rows into 256 B shares: pack reads whole rows
-    "pack_rows_tp2_to_tp4": _custom(num_layers=4, num_kv_heads=4, head_dim=128, old_topo=(2, 1), new_topo=(4, 1)),
-    "pack_rows_4way_reblock": _custom(num_layers=3, num_kv_heads=4, head_dim=128, old_topo=(1, 1),
-                                      new_topo=(4, 1), old_block_size=16, new_block_size=32),
-    "short_row_shares_fp8": _custom(num_layers=4, num_kv_heads=32, head_dim=128, elem_bytes=1,
-                                    old_topo=(8, 1), new_topo=(2, 2), old_block_size=16, new_block_size=32),
-    # explicit uneven pipeline partitions
-    "uneven_pp": _custom(num_layers=5, old_topo=(2, 2, (0, 3, 5)), new_topo=(1, 3, (0, 1, 2, 5))),
-    "uneven_to_even": _custom(num_layers=6, old_topo=(1, 4, (0, 1, 3, 4, 6)), new_topo=(2, 2),
-                              new_block_size=32),
-}
-
 
 @pytest.mark.parametrize("name", list(EDGE))
 def test_edge_case(name):

@@ -31,7 +31,12 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
 PEAK_PCIE_GBS = 64.0   # PCIe Gen5 x16, one direction (32 GT/s x 16 lanes)
-COUNTERS = os.path.join(ROOT, "profiles", "copy_slices_gqa70b_hbm_counters.json")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def counters_path(workload: str) -> str:
+    """The committed HBM counter record of a workload's pack and unpack calls."""
+    return os.path.join(PROFILES, f"hbm_counters_{workload}.json")
 CSRC = os.path.join(ROOT, "paper_2606_18741_amd", "csrc")
 KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("device_util.hpp", "kv_copy.hpp", "kv_device.hpp", "kv_expand.hpp",
                                                   "kv_rows.hpp", "kv_tiles.hpp", "migrate.hip")]
@@ -68,6 +73,23 @@ def parse():
                     help="layers per window for the layer-streaming measurement, comma separated ('' to skip)")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (for counter scaling), then exit")
+    ap.add_argument("--library-calibration", type=float, default=0.0, metavar="GIB",
+                    help="only run the library's pack on a contiguous pool of this many GiB (one sequence over "
+                         "blocks 0..n-1, identity topology: every byte read and written once, in order), then exit")
+    ap.add_argument("--counter-pass", action="store_true",
+                    help="only build the share and run 3 pack and 3 unpack calls (for rocprofv3 --pmc), then exit")
+    ap.add_argument("--summarize-counters", nargs=4, default=None,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
+                    help="write profiles/hbm_counters_<workload>.json from rocprofv3 counter CSVs of a --counter-pass "
+                         "run (FETCH_SIZE, WRITE_SIZE) and of a --library-calibration run (same counters), then exit")
+    ap.add_argument("--summarize-trace", default=None, metavar="STATS_CSV",
+                    help="print a markdown table of a rocprofv3 --stats kernel summary (the library's kernels), "
+                         "then exit")
+    ap.add_argument("--calibration-gib", type=float, default=4.0,
+                    help="size of the --library-calibration pool that the summarized calibration CSVs came from")
+    ap.add_argument("--ceiling", type=float, default=0.0, metavar="GIB",
+                    help="only run the HBM access-pattern probes (libremp_probe.so) over buffers of this many GiB, "
+                         "then exit")
     return ap.parse_args()
 
 
@@ -95,11 +117,11 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def profiled_call(kernel: str):
-    """The committed counter record of the `kernel` call ("pack" / "unpack"), if it was taken on this
-    kernel source: HBM bytes per call, the kernel it launches and its launches per call; else None."""
+def profiled_call(workload: str, kernel: str):
+    """The committed counter record of the workload's `kernel` call ("pack" / "unpack"), if it was taken on
+    this kernel source: HBM bytes per call, the kernel it launches and its launches per call; else None."""
     try:
-        with open(COUNTERS) as f:
+        with open(counters_path(workload)) as f:
             c = json.load(f)
     except (OSError, ValueError):
         return None
@@ -125,6 +147,223 @@ def copy_calibration(gib: float) -> None:
     ms = e0.elapsed_time(e1) / reps
     print(json.dumps({"copy_bytes_per_launch_read": n, "copy_bytes_per_launch_write": n, "launches": reps,
                       "ms_per_copy": round(ms, 4), "copy_GBps_read_plus_write": round(2 * n / ms / 1e6, 1)}))
+
+
+def _calibration_bytes(gib: float) -> int:
+    """Bytes the library-calibration pack reads (and writes): K and V of a pool of `gib` GiB, 4 KiB blocks."""
+    nblk = int(gib * (1 << 30)) // (2 * 16 * 256)
+    return 2 * nblk * 16 * 256
+
+
+def library_calibration(gib: float) -> int:
+    """The library's pack over a contiguous pool: identity topology, one head, one sequence whose table is
+    blocks 0..n-1 in order, so the pack kernel reads the whole pool and writes the whole staging buffer once,
+    both in address order.  Counter readings of this launch against its known bytes scale FETCH_SIZE and
+    WRITE_SIZE for the library's own 16-byte non-temporal accesses."""
+    import numpy as np
+    import torch
+
+    import paper_2606_18741_amd as rk
+    from paper_2606_18741_amd import torch_io as tio
+
+    bs, D = 16, 128
+    row = D * 2
+    nblk = int(gib * (1 << 30)) // (2 * bs * row)          # K and V pools together hold `gib` GiB
+    T = nblk * bs
+    lens = np.array([T], np.int32)
+    tables = rk.HostTables(lens, np.array([0, nblk], np.int32), np.arange(nblk, dtype=np.int32), nblk)
+    plan = rk.Plan((1, 1), (1, 1), (1, 1, D, 2, bs, bs), tables)
+    pool = torch.empty((2, nblk, bs, 1, D), dtype=torch.int16, device="cuda")
+    pool.fill_(3)
+    stage = torch.empty(plan.pairs[0].staging_bytes, dtype=torch.uint8, device="cuda")
+    dt = tio.DeviceTables(tables)
+    ws = tio.workspace(plan)
+    arg = tio.pool_arg([pool], nblk)
+    st = tio.staging_args({(0, 0): stage}, 0, 1, as_src=True)
+    stream = tio.current_stream()
+    reps = 5
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    plan.pack(0, arg, dt.dev, st, ws, ws.numel(), stream)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        plan.pack(0, arg, dt.dev, st, ws, ws.numel(), stream)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    if tio.workspace_flag(ws) != 0 or not torch.equal(stage.view(torch.int16), pool.reshape(-1)):
+        print("library calibration: the staging buffer is not the pool", file=sys.stderr)
+        return 1
+    n = stage.numel()
+    print(json.dumps({"kind": "library pack, contiguous", "bytes_read_per_call": n, "bytes_written_per_call": n,
+                      "calls": reps + 1, "ms_per_call": round(ms, 4), "GBps_read_plus_write": round(2 * n / ms / 1e6, 1)}))
+    return 0
+
+
+def _counter_rows(path: str):
+    """(dispatch id, kernel name, counter name, value) of a rocprofv3 counter-collection CSV, in dispatch order."""
+    import csv
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"])))
+    rows.sort()
+    return rows
+
+
+def _calls(rows):
+    """Split a counter-pass dispatch sequence into library calls: every call starts with expand_scan; a call
+    with a sort is an unpack, else a pack.  Returns [(kind, [(kernel, value) of its copy launches])]."""
+    calls = []
+    for _, name, _, value in rows:
+        if "remp::" not in name:
+            continue
+        if "expand_scan" in name:
+            calls.append(["pack", []])
+        elif not calls:
+            continue
+        elif "sort_scan" in name:
+            calls[-1][0] = "unpack"
+        elif "copy_" in name:
+            calls[-1][1].append((name, value))
+    return calls
+
+
+def summarize_counters(args) -> int:
+    """profiles/hbm_counters_<workload>.json from a --counter-pass run's FETCH_SIZE and WRITE_SIZE CSVs
+    (the last three packs and three unpacks) scaled by a --library-calibration run's readings."""
+    import paper_2606_18741_amd as rk
+    import synthkv
+    fetch_csv, write_csv, cal_fetch_csv, cal_write_csv = args.summarize_counters
+    w = synthkv.WORKLOADS[args.workload]
+    inp = synthkv.make_inputs(w)
+    plan = rk.Plan(w.old_topo, w.new_topo, (w.num_layers, w.num_kv_heads, w.head_dim, w.elem_bytes,
+                                           w.old_block_size, w.new_block_size), rk.HostTables.of(inp.old_tables))
+    ro, qn = w.role
+    P_pack = sum(p.staging_bytes for p in plan.pairs if p.src == ro)
+    P_unpack = sum(p.staging_bytes for p in plan.pairs if p.dst == qn)
+
+    def calib(path, which):
+        calls = _calls(_counter_rows(path))
+        vals = [sum(v for _, v in c[1]) for c in calls if c[1]]
+        return calls[-1][1][0][0], statistics.median(vals)
+
+    # the calibration pool: K and V of args.library_calibration-sized pool, read once and written once
+    cal_kernel, cal_fetch = calib(cal_fetch_csv, "fetch")
+    _, cal_write = calib(cal_write_csv, "write")
+    cal_bytes = _calibration_bytes(args.calibration_gib)
+    fetch_scale = cal_bytes / (cal_fetch * 1024)
+    write_scale = cal_bytes / (cal_write * 1024)
+    out = {"workload": w.name + ": " + w.description, "source_hash": source_hash(),
+           "note": "counters of the last 3 pack and 3 unpack calls of a --counter-pass run, summed over the copy "
+                   "launches of a call (a call launches once per 8 slices, or per 8 layers for whole rows), "
+                   "median over calls, KiB scaled by the library-calibration factors",
+           "commands": [f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc/{w.name}_fetch -o f -- "
+                        f"python bench.py --workload {w.name} --counter-pass",
+                        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc/{w.name}_write -o w -- "
+                        f"python bench.py --workload {w.name} --counter-pass",
+                        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc/cal_fetch -o f -- "
+                        f"python bench.py --library-calibration {args.calibration_gib}",
+                        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc/cal_write -o w -- "
+                        f"python bench.py --library-calibration {args.calibration_gib}",
+                        f"python bench.py --workload {w.name} --calibration-gib {args.calibration_gib} "
+                        f"--summarize-counters <the four CSVs>"],
+           "calibration": {"kernel": cal_kernel, "known_bytes_read": cal_bytes, "known_bytes_written": cal_bytes,
+                           "fetch_size_kib": round(cal_fetch, 1), "write_size_kib": round(cal_write, 1),
+                           "fetch_scale": round(fetch_scale, 5), "write_scale": round(write_scale, 5)},
+           "kernels": {}}
+    fetch_calls = _calls(_counter_rows(fetch_csv))
+    write_calls = _calls(_counter_rows(write_csv))
+    for kind, algo in (("pack", 2 * P_pack), ("unpack", 2 * P_unpack)):
+        fc = [c for c in fetch_calls if c[0] == kind and c[1]][-3:]
+        wc = [c for c in write_calls if c[0] == kind and c[1]][-3:]
+        f_kib = statistics.median(sum(v for _, v in c[1]) for c in fc)
+        w_kib = statistics.median(sum(v for _, v in c[1]) for c in wc)
+        hbm = f_kib * 1024 * fetch_scale + w_kib * 1024 * write_scale
+        out["kernels"][kind] = {"kernel": fc[-1][1][0][0], "launches_per_call": len(fc[-1][1]), "calls": len(fc),
+                                "fetch_size_kib_per_call": round(f_kib, 1), "write_size_kib_per_call": round(w_kib, 1),
+                                "hbm_bytes_per_call": int(hbm), "algorithmic_bytes_per_call": algo,
+                                "hbm_over_algorithmic": round(hbm / algo, 5)}
+    with open(counters_path(w.name), "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out["kernels"]))
+    return 0
+
+
+def summarize_trace(path: str) -> int:
+    """Markdown table of the library's kernels in a rocprofv3 kernel-stats CSV: calls, average and total time."""
+    import csv
+    with open(path) as f:
+        rows = [r for r in csv.DictReader(f) if "remp::" in r["Name"] or "probe" in r["Name"]]
+    print("| kernel | calls | average (ms) | total (ms) |")
+    print("|---|---|---|---|")
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = r["Name"].replace("void ", "").replace("remp::", "").split("(")[0]
+        print(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | {float(r['TotalDurationNs']) / 1e6:.3f} |")
+    return 0
+
+
+def ceiling(gib: float) -> int:
+    """HBM access-pattern probes: 4 and 8 KiB chunks copied, read or written in address order or through a
+    random permutation, each at every launch shape, median of 3 launches; GB/s counts bytes read plus
+    bytes written."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_18741_amd", "libremp_probe.so"))
+    fn = lib.remp_probe_chunks
+    fn.restype = ctypes.c_int32
+    fn.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_void_p]
+    stream = torch.cuda.current_stream()
+    shapes = [(t, u, c) for t in (256, 512, 1024) for u in (1, 2, 4, 8) for c in (1, 2, 4, 16)]
+    patterns = [("copy, contiguous", 0, False, False), ("copy, random reads (gather)", 0, True, False),
+                ("copy, random writes (scatter)", 0, False, True), ("copy, random reads and writes", 0, True, True),
+                ("read only, contiguous", 1, False, False), ("read only, random", 1, True, False),
+                ("write only, contiguous", 2, False, False), ("write only, random", 2, False, True)]
+    results = []
+    for chunk in (4096, 8192):
+        n = int(gib * (1 << 30)) // chunk
+        src = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
+        dst = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
+        src.fill_(1)
+        dst.fill_(2)
+        g = torch.Generator(device="cpu").manual_seed(chunk)
+        perm_r = torch.randperm(n, generator=g).to(torch.int32).cuda()
+        perm_w = torch.randperm(n, generator=g).to(torch.int32).cuda()
+        sink = torch.empty(1024 * 16, dtype=torch.uint8, device="cuda")
+        for name, mode, rr, rw in patterns:
+            moved = (2 if mode == 0 else 1) * n * chunk
+            best = None
+            for (t, u, c) in shapes:
+                args = (mode, src.data_ptr(), dst.data_ptr(), sink.data_ptr(), sink.numel(), n, chunk,
+                        perm_r.data_ptr() if rr else None, perm_w.data_ptr() if rw else None, t, u, c,
+                        stream.cuda_stream)
+                if -(-n // c) * t >= (1 << 32):
+                    continue                      # more work-items than one dispatch counts
+                if fn(*args) != 0:
+                    raise RuntimeError(f"probe launch refused: {name} {t}x{u} cpw {c}")
+                ts = []
+                for _ in range(3):
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    fn(*args)
+                    e1.record()
+                    e1.synchronize()
+                    ts.append(e0.elapsed_time(e1))
+                gbps = moved / statistics.median(ts) / 1e6
+                if best is None or gbps > best[0]:
+                    best = (gbps, t, u, c)
+            results.append({"chunk_bytes": chunk, "pattern": name, "GBps": round(best[0], 1),
+                            "frac_of_peak": round(best[0] / PEAK_HBM_GBS, 4),
+                            "best_shape": {"threads": best[1], "unroll": best[2], "chunks_per_workgroup": best[3]}})
+            log(f"ceiling {chunk} B {name}: {best[0]:.1f} GB/s ({best[1]} x {best[2]}, {best[3]} chunks per workgroup)")
+        del src, dst, perm_r, perm_w, sink
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "HBM access-pattern ceiling", "unit": "GB/s (read + write)", "buffer_GiB": gib,
+                      "shapes_tried": len(shapes), "results": results}))
+    return 0
 
 
 # KV workload -> the decoder whose weights the same switch rebuilds
@@ -220,6 +459,14 @@ def main() -> int:
     if args.copy_calibration > 0:
         copy_calibration(args.copy_calibration)
         return 0
+    if args.ceiling > 0:
+        return ceiling(args.ceiling)
+    if args.library_calibration > 0:
+        return library_calibration(args.library_calibration)
+    if args.summarize_counters:
+        return summarize_counters(args)
+    if args.summarize_trace:
+        return summarize_trace(args.summarize_trace)
 
     import numpy as np
     import torch
@@ -364,6 +611,16 @@ def main() -> int:
         ms = start.elapsed_time(stop) / max(args.steps, 1)
         return ms, [e[0].elapsed_time(e[1]) for e in evs], [e[2].elapsed_time(e[3]) for e in evs]
 
+    if args.counter_pass:
+        # the calls rocprofv3 --pmc reads: the share's pack and unpack, three times each
+        sh = build(keep_host=False)
+        for _ in range(3):
+            step(sh)
+        torch.cuda.synchronize()
+        if tio.workspace_flag(sh.ws) != 0:
+            raise RuntimeError("device tables disagree with host tables")
+        log("counter pass: 3 pack and 3 unpack calls done")
+        return 0
     first_touch = None
     if not args.no_first_touch:
         # the same steps on a share allocated before any prewarm of device memory
@@ -482,7 +739,7 @@ def main() -> int:
     else:
         dom, dom_ms, dom_bytes = "unpack", unpack_avg, 2 * P_unpack
     achieved = dom_bytes / (dom_ms / 1e3) / 1e9
-    prof = profiled_call(dom)
+    prof = profiled_call(w.name, dom)
     kname = prof["kernel"].replace("void remp::", "").split("<")[0] if prof else "copy kernel"
     roofline = {
         "bound": "hbm",

@@ -1,0 +1,46 @@
+/*
+ * remp_probe.h -- HBM access-pattern probes for gfx950 (measurement only).
+ *
+ * The KV migration reads and writes paged blocks of 4-64 KiB at scattered
+ * places (a serving engine's block tables come from a free list).  These
+ * probes measure what the memory system sustains for such patterns on its
+ * own, so the migration's kernels can be placed against a practical ceiling
+ * next to the 8 TB/s peak.  They live in their own library, libremp_probe.so,
+ * and never run as part of a migration.
+ */
+#ifndef REMP_PROBE_H
+#define REMP_PROBE_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REMP_PROBE_API __attribute__((visibility("default")))
+
+/* Enqueue one probe launch on `stream`.  The chunk list has n_chunks entries;
+ * entry i touches chunk src_idx[i] of src and chunk dst_idx[i] of dst
+ * (chunk c is bytes [c * chunk_bytes, (c + 1) * chunk_bytes)); a NULL index
+ * array means the identity.  mode 0 copies each source chunk to its
+ * destination chunk, mode 1 only reads the source chunks (each lane folds
+ * what it read into a value that a store to `sink`, threads * 16 bytes of
+ * device memory, would write on a condition that practically never holds),
+ * mode 2 only writes the destination chunks.  All accesses are 16-byte non-temporal loads and stores.
+ * chunk_bytes: a power of two >= 16.  threads: 256, 512 or 1024; unroll
+ * (16-byte vectors in flight per lane): 1, 2, 4 or 8; chunks_per_wg >= 1;
+ * ceil(n_chunks / chunks_per_wg) * threads below 2^32.
+ * The caller guarantees that src, dst (device, 16-byte aligned) hold every
+ * chunk the index arrays (device, n_chunks int32 each) name.  Returns 0, -1
+ * for an invalid argument (nothing enqueued), -2 for a launch error. */
+REMP_PROBE_API int32_t remp_probe_chunks(int32_t mode, const void* src, void* dst, void* sink, int64_t sink_bytes,
+                                         int64_t n_chunks, int32_t chunk_bytes, const int32_t* src_idx,
+                                         const int32_t* dst_idx, int32_t threads, int32_t unroll,
+                                         int32_t chunks_per_wg, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REMP_PROBE_H */

@@ -1,4 +1,5 @@
-"""Build libremp_kv.so (KV migration and weight-shard rebuild) for gfx950 in-tree with hipcc.
+"""Build libremp_kv.so (KV migration and weight-shard rebuild) and libremp_probe.so (HBM access-pattern
+probes, measurement only) for gfx950 in-tree with hipcc.
 
     python paper_2606_18741_amd/build.py      (a plain script: importing the package needs the library)
 """
@@ -13,8 +14,10 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libremp_kv.so")
+PROBE_LIB = os.path.join(PKG, "libremp_probe.so")
 
 SOURCES = [os.path.join(CSRC, f) for f in ("plan.cpp", "migrate.hip", "weights_plan.cpp", "weights.hip")]
+PROBE_SOURCES = [os.path.join(CSRC, "probe.hip")]   # HBM access-pattern probes (measurement only)
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",
@@ -39,12 +42,11 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source into LIB (always recompiles).  Returns the library path."""
-    tmp = LIB + ".tmp"
+def _link(sources, out: str, verbose: bool) -> str:
+    tmp = out + ".tmp"
     rocm_inc = os.path.join(os.path.dirname(os.path.dirname(hipcc())), "include")
     cmd = [hipcc(), *HIPCC_FLAGS, "-I", rocm_inc, "-o", tmp]
-    for src in SOURCES:
+    for src in sources:
         if src.endswith(".hip"):
             cmd += ["-x", "hip", src]
         else:
@@ -56,7 +58,15 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{res.stdout}\n{res.stderr}")
     if verbose and res.stderr.strip():
         print(res.stderr, file=sys.stderr)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Compile LIB from every library source and PROBE_LIB from the probes (always recompiles).
+    Returns the library path."""
+    _link(SOURCES, LIB, verbose)
+    _link(PROBE_SOURCES, PROBE_LIB, verbose)
     return LIB
 
 

@@ -49,6 +49,14 @@ static int64_t wg_target(const remp_kv_plan_t& p, int64_t builtin) { return p.wg
 // Bound on a copy workgroup's flattened (unit, row, vector) index space.
 constexpr uint64_t kMaxWgVectors = uint64_t(1) << 31;
 
+// A dispatch counts its work-items in 32 bits per grid dimension, and the XCD cell order numbers the
+// workgroups of a launch linearly in 32 bits.
+static remp_status check_grid(int64_t gx, int64_t gy, int threads, const char* what) {
+    if (gx * threads >= (int64_t(1) << 32) || gx * gy >= (int64_t(1) << 32))
+        return fail(REMP_E_UNSUPPORTED, std::string(what) + ": too many workgroups for one launch");
+    return REMP_OK;
+}
+
 struct HostSlice {
     uint64_t paged_k, paged_v, stage;
     uint32_t row_bytes;
@@ -193,8 +201,8 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     a.block_size = bs;
     a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
-    if (gx * kMaxItems >= (int64_t(1) << 32))
-        return fail(REMP_E_UNSUPPORTED, "too many block descriptors for one launch");
+    const int threads = small ? (PACK ? kPackSmallThreads : kSmallThreads) : kLargeThreads;
+    if (remp_status st = check_grid(gx, kMaxItems, threads, PACK ? "pack" : "unpack")) return st;
 
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
@@ -252,7 +260,7 @@ static remp_status launch_tiles(const remp_kv_plan_t& p, const std::vector<HostS
     const int32_t tpw = static_cast<int32_t>(std::max<int64_t>(
         1, std::min<int64_t>({kTileWgBytes / tile_bytes, kTileLdsBytes / tile_lds, int64_t(kMaxUnitsPerWg)})));
     const int64_t gx = (n_desc * 2 * max_hc + tpw - 1) / tpw;
-    if (gx > 0x7FFFFFFF) return fail(REMP_E_UNSUPPORTED, "too many tiles for one launch");
+    if (remp_status st = check_grid(gx, kMaxItems, kTileThreads, "head tiles")) return st;
 
     TileArgs a;
     std::memset(&a, 0, sizeof(a));
@@ -384,6 +392,8 @@ static remp_status launch_rows(const remp_kv_plan_t& p, const std::vector<std::v
     a.vps_magic = fv.magic;
     a.vps_shift = fv.shift;
     const int64_t gx = (2 * n_desc + C - 1) / C;
+    if (remp_status st = check_grid(gx, kMaxMergeGroups, small ? kRowsSmallThreads : kLargeThreads, "whole rows"))
+        return st;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
     }
@@ -661,7 +671,7 @@ static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector
             max_hc = std::max(max_hc, c.heads);
         }
         const int64_t gx = (n_desc * 2 * max_hc + T - 1) / T;
-        if (gx > 0x7FFFFFFF) return fail(REMP_E_UNSUPPORTED, "too many head tiles for one launch");
+        if (remp_status st = check_grid(gx, kMaxLocalTileItems, kTileThreads, "local head tiles")) return st;
         // 32-bit vector indices per workgroup: T tiles of bn rows of hb / 16 vectors
         hipLaunchKernelGGL(copy_local_tiles, dim3(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt)),
                            dim3(kTileThreads), static_cast<size_t>(T * tile_lds), stream, a);
@@ -718,6 +728,8 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     a.new_block_size = bn;
     a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
+    if (remp_status st = check_grid(gx, kMaxLocalItems, small ? kSmallThreads : kLocalLargeThreads, "local copy"))
+        return st;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;
     }

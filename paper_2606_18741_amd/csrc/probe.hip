@@ -1,0 +1,118 @@
+// Access-pattern probes for gfx950 HBM: chunk copies, reads and writes in any
+// chunk order, to measure what the memory system sustains for the patterns the
+// KV migration produces (contiguous, gathered and scattered 4-8 KiB pieces).
+// Measurement infrastructure only: built into its own library
+// (libremp_probe.so), never called by the migration.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "remp_probe.h"
+
+namespace {
+
+typedef unsigned int V4 __attribute__((ext_vector_type(4)));
+
+// One workgroup takes `cpw` consecutive entries of the chunk list; its lanes
+// stride over the (chunk, 16-byte vector) space with UNROLL vectors in flight.
+// Entry i moves chunk src_idx[i] of src to chunk dst_idx[i] of dst (identity
+// when an index array is NULL).  MODE 0 copies, 1 only reads (each lane folds what
+// it read into a register that a practically never taken store keeps alive), 2 only writes.
+template <int THREADS, int UNROLL, int MODE>
+__global__ __launch_bounds__(THREADS) void chunk_probe(const char* __restrict__ src, char* __restrict__ dst,
+                                                       V4* __restrict__ sink, int64_t n_chunks, uint32_t chunk_vecs,
+                                                       uint32_t vec_shift, const int32_t* __restrict__ src_idx,
+                                                       const int32_t* __restrict__ dst_idx, int32_t cpw) {
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * cpw;
+    const int64_t nc = min(static_cast<int64_t>(cpw), n_chunks - c0);
+    if (nc <= 0) return;
+    const uint32_t total = static_cast<uint32_t>(nc) * chunk_vecs;
+    const uint64_t chunk_bytes = static_cast<uint64_t>(chunk_vecs) * 16;
+    V4 acc = {0u, 0u, 0u, 0u};
+    for (uint32_t base = threadIdx.x; base < total; base += THREADS * UNROLL) {
+        V4 r[UNROLL];
+        uint64_t d[UNROLL];
+        bool ok[UNROLL];
+#pragma unroll
+        for (int j = 0; j < UNROLL; ++j) {
+            const uint32_t x = base + j * THREADS;
+            ok[j] = x < total;
+            d[j] = 0;
+            if (ok[j]) {
+                const int64_t c = c0 + (x >> vec_shift);
+                const uint32_t v = x & (chunk_vecs - 1);
+                const int64_t sc = src_idx ? src_idx[c] : c;
+                const int64_t dc = dst_idx ? dst_idx[c] : c;
+                d[j] = static_cast<uint64_t>(dc) * chunk_bytes + v * 16;
+                if (MODE != 2)
+                    r[j] = __builtin_nontemporal_load(
+                        reinterpret_cast<const V4*>(src + static_cast<uint64_t>(sc) * chunk_bytes + v * 16));
+                else
+                    r[j] = V4{x, 1u, 2u, 3u};
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < UNROLL; ++j) {
+            if (!ok[j]) continue;
+            if (MODE == 1) acc ^= r[j];
+            else __builtin_nontemporal_store(r[j], reinterpret_cast<V4*>(dst + d[j]));
+        }
+    }
+    // keeps the loads of the read-only probe alive; the stored value is practically never reached
+    if (MODE == 1 && acc.x == 0x9E3779B9u && acc.y == 0x7F4A7C15u && acc.z == 0x85EBCA6Bu) sink[threadIdx.x] = acc;
+}
+
+template <int THREADS, int UNROLL>
+hipError_t launch_mode(int32_t mode, dim3 grid, const char* src, char* dst, V4* sink, int64_t n, uint32_t cv,
+                       uint32_t sh, const int32_t* si, const int32_t* di, int32_t cpw, hipStream_t s) {
+    if (mode == 0) hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 0>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
+    else if (mode == 1) hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 1>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
+    else hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 2>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
+    return hipGetLastError();
+}
+
+template <int THREADS>
+hipError_t launch_unroll(int32_t unroll, int32_t mode, dim3 grid, const char* src, char* dst, V4* sink, int64_t n,
+                         uint32_t cv, uint32_t sh, const int32_t* si, const int32_t* di, int32_t cpw, hipStream_t s) {
+    switch (unroll) {
+        case 1: return launch_mode<THREADS, 1>(mode, grid, src, dst, sink, n, cv, sh, si, di, cpw, s);
+        case 2: return launch_mode<THREADS, 2>(mode, grid, src, dst, sink, n, cv, sh, si, di, cpw, s);
+        case 4: return launch_mode<THREADS, 4>(mode, grid, src, dst, sink, n, cv, sh, si, di, cpw, s);
+        default: return launch_mode<THREADS, 8>(mode, grid, src, dst, sink, n, cv, sh, si, di, cpw, s);
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t remp_probe_chunks(int32_t mode, const void* src, void* dst, void* sink, int64_t sink_bytes,
+                          int64_t n_chunks, int32_t chunk_bytes, const int32_t* src_idx, const int32_t* dst_idx,
+                          int32_t threads, int32_t unroll, int32_t chunks_per_wg, hipStream_t stream) {
+    if (mode < 0 || mode > 2) return -1;
+    if (n_chunks <= 0 || chunk_bytes < 16 || (chunk_bytes & (chunk_bytes - 1)) != 0) return -1;
+    if (threads != 256 && threads != 512 && threads != 1024) return -1;
+    if (unroll != 1 && unroll != 2 && unroll != 4 && unroll != 8) return -1;
+    if (chunks_per_wg < 1) return -1;
+    const uint32_t cv = static_cast<uint32_t>(chunk_bytes / 16);
+    uint32_t sh = 0;
+    while ((1u << sh) < cv) ++sh;
+    if (static_cast<uint64_t>(chunks_per_wg) * cv + static_cast<uint64_t>(threads) * unroll >= (uint64_t(1) << 31))
+        return -1;
+    const int64_t grid = (n_chunks + chunks_per_wg - 1) / chunks_per_wg;
+    if (grid * threads >= (int64_t(1) << 32)) return -1;   // work-items of a dispatch are counted in 32 bits
+    if (mode != 2 && !src) return -1;
+    if (mode != 1 && !dst) return -1;
+    if (mode == 1 && (!sink || sink_bytes < static_cast<int64_t>(threads) * 16)) return -1;
+    const dim3 g(static_cast<uint32_t>(grid));
+    const char* s = static_cast<const char*>(src);
+    char* d = static_cast<char*>(dst);
+    V4* k = static_cast<V4*>(sink);
+    hipError_t e;
+    if (threads == 256) e = launch_unroll<256>(unroll, mode, g, s, d, k, n_chunks, cv, sh, src_idx, dst_idx, chunks_per_wg, stream);
+    else if (threads == 512) e = launch_unroll<512>(unroll, mode, g, s, d, k, n_chunks, cv, sh, src_idx, dst_idx, chunks_per_wg, stream);
+    else e = launch_unroll<1024>(unroll, mode, g, s, d, k, n_chunks, cv, sh, src_idx, dst_idx, chunks_per_wg, stream);
+    return e == hipSuccess ? 0 : -2;
+}
+
+}  // extern "C"

@@ -2,6 +2,8 @@
 model of the kernels."""
 from __future__ import annotations
 
+import numpy as np
+
 import synthkv
 
 
@@ -51,3 +53,30 @@ EDGE = {
     "uneven_to_even": custom(num_layers=6, old_topo=(1, 4, (0, 1, 3, 4, 6)), new_topo=(2, 2),
                               new_block_size=32),
 }
+
+
+# Pool layout pairs (old, new) of the shifted-lengths case: NHD, HND and ROCm tiles, same and mixed.
+SHIFTED_LAYOUTS = [(0, 0), (1, 1), (2, 2), (0, 1)]
+
+
+def shifted_old_lengths_case():
+    """Identity topology (every slice is local) and old device tables that disagree with the host ones:
+    17 tokens move from sequence 1 to sequence 0 (same total, shifted starts), and sequence 1's first old
+    block is physical block 0.  The local copies combine the new expansion's token offsets with the old
+    one's, so the first 16 rows of sequence 1 get a negative token index.  Returns (workload, inputs,
+    (device lengths, device row offsets, device block ids))."""
+    w = custom(num_layers=2, num_kv_heads=8, head_dim=64, old_topo=(2, 1), new_topo=(2, 1), num_seqs=3,
+               length_law=("fixed", 40), seed=5)
+    inp = synthkv.make_inputs(w)
+    t = inp.old_tables
+    lens = t.seq_lens.copy()
+    lens[0] += 17
+    lens[1] -= 17
+    ids = t.ids.copy()
+    first1 = int(t.offsets[1])
+    zero = np.nonzero(ids == 0)[0]
+    if zero.size:
+        ids[zero[0]], ids[first1] = ids[first1], 0
+    else:
+        ids[first1] = 0
+    return w, inp, (lens, t.offsets.copy(), ids)

@@ -1,9 +1,26 @@
 """Seeded random KV-migration configurations for the GPU fuzz tests (inputs only)."""
 from __future__ import annotations
 
+import os
+
 import numpy as np
 
 import synthkv
+
+
+def seed_range(default_stop: int):
+    """Seeds of the random configurations: range(0, default_stop), or REMP_FUZZ_SEEDS="start:stop" to run
+    another range of the same generator (longer runs outside the default suite)."""
+    spec = os.environ.get("REMP_FUZZ_SEEDS")
+    if spec:
+        a, b = spec.split(":")
+        return range(int(a), int(b))
+    return range(default_stop)
+
+
+def layout_count(default: int) -> int:
+    """Number of layout cases: `default`, or REMP_FUZZ_LAYOUT_CASES."""
+    return int(os.environ.get("REMP_FUZZ_LAYOUT_CASES", default))
 
 
 def random_workload(seed: int) -> synthkv.KVWorkload:

@@ -104,6 +104,12 @@ def cdiv_trunc(a: np.ndarray, b: int) -> np.ndarray:
     return np.sign(a) * (np.abs(a) // b)
 
 
+def check_grid(gx: int, gy: int, threads: int, what: str) -> None:
+    """The launch code's refusal of grids whose work-items or workgroups overflow 32 bits."""
+    if gx * threads >= (1 << 32) or gx * gy >= (1 << 32):
+        raise ModelError(f"unsupported: {what}: too many workgroups for one launch")
+
+
 def lowest_bit(x: int) -> int:
     return x & -x
 
@@ -385,6 +391,7 @@ def copy_launches(slices: Sequence[Slice], n_desc: int, bs: int, block_stride: i
         raise ModelError("unsupported: a block exceeds the workgroup index space")
     gx = (2 * n_desc + C - 1) // C
     shape = (PACK_SMALL if pack else UNPACK_SMALL) if small else LARGE
+    check_grid(gx, MAX_ITEMS, shape[0], "copy")
     out = []
     for f in range(0, len(slices), MAX_ITEMS):
         group = list(slices[f:f + MAX_ITEMS])
@@ -441,6 +448,7 @@ def rows_launches(groups: List[List[Slice]], n_desc: int, bs: int, block_stride:
     if bs * (row_stride // vec) >= MAX_WG_VECTORS:
         raise ModelError("unsupported: a block of one row exceeds the workgroup index space")
     gx = (2 * n_desc + C - 1) // C
+    check_grid(gx, MAX_MERGE_GROUPS, (ROWS_SMALL if small else ROWS_LARGE)[0], "whole rows")
     out = []
     for f in range(0, len(groups), MAX_MERGE_GROUPS):
         gg = groups[f:f + MAX_MERGE_GROUPS]
@@ -468,6 +476,7 @@ def tile_launches(slices: Sequence[Slice], n_desc: int, bs: int, block_stride: i
         raise ModelError("unsupported: a tile does not fit in LDS")
     tpw = max(1, min(TILE_WG_BYTES // tile_bytes, TILE_LDS_BYTES // tile_lds, MAX_UNITS_PER_WG))
     gx = (n_desc * 2 * max_hc + tpw - 1) // tpw
+    check_grid(gx, MAX_ITEMS, TILE_THREADS, "head tiles")
     out = []
     for f in range(0, len(slices), MAX_ITEMS):
         group = list(slices[f:f + MAX_ITEMS])
@@ -509,6 +518,7 @@ def local_launches(items: Sequence[LocalItem], n_new: int, bo: int, bn: int, oro
     if bn * (max_row // vec) >= MAX_WG_VECTORS:
         raise ModelError("unsupported: a block exceeds the workgroup index space")
     gx = (2 * n_new + C - 1) // C
+    check_grid(gx, MAX_LOCAL_ITEMS, (LOCAL_SMALL if small else LOCAL_LARGE)[0], "local copy")
     out = []
     for f in range(0, len(items), MAX_LOCAL_ITEMS):
         group = list(items[f:f + MAX_LOCAL_ITEMS])
@@ -536,6 +546,7 @@ def local_tile_launches(items: Sequence[LocalItem], n_new: int, bo: int, bn: int
         group = list(items[f:f + MAX_LOCAL_ITEMS])
         max_hc = max(1, max(it.row_bytes // hb for it in group))
         gx = (n_new * 2 * max_hc + T - 1) // T
+        check_grid(gx, MAX_LOCAL_ITEMS, TILE_THREADS, "local head tiles")
         out.append(Launch("copy_local_tiles", (gx, len(group)), TILE_THREADS, 1, False,
                           args=dict(items=group, T=T, bo=bo, bn=bn, hb=hb, eb=eb, lo=lo, ln=ln, lrow=lrow,
                                     orow=orow, nrow=nrow, n_new=n_new,

@@ -62,6 +62,26 @@ def test_exports_every_declared_symbol():
         assert rk.remp_status_string(code) == name
 
 
+def test_probe_library_exports_and_refuses_bad_arguments():
+    """libremp_probe.so (HBM access-pattern probes, measurement only) exports its one entry point and refuses
+    invalid arguments before touching the GPU."""
+    import ctypes
+    import subprocess
+    path = os.path.join(os.path.dirname(rk._lib._LIB_PATH), "libremp_probe.so")
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True).stdout
+    assert {ln.split()[-1] for ln in out.splitlines() if "remp_" in ln} == {"remp_probe_chunks"}
+    fn = ctypes.CDLL(path).remp_probe_chunks
+    fn.restype = ctypes.c_int32
+    fn.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_void_p]
+    ok = (0, 1 << 40, 1 << 41, None, 0, 16, 4096, None, None, 256, 2, 1, None)
+    for i, bad in ((0, 3), (6, 4000), (9, 128), (10, 3), (11, 0), (5, 0)):
+        a = list(ok)
+        a[i] = bad
+        assert fn(*a) == -1, (i, bad)
+
+
 def test_only_the_abi_is_exported_from_host_code():
     import subprocess
     out = subprocess.run(["nm", "-D", "--defined-only", rk._lib._LIB_PATH], capture_output=True, text=True).stdout

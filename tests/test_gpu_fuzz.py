@@ -14,15 +14,13 @@ from __future__ import annotations
 import pytest
 
 import synthkv
-from fuzzcases import layout_cases, random_windows, random_workload
+from fuzzcases import layout_cases, layout_count, random_windows, random_workload, seed_range
 from test_gpu_parity import _layouts_case, _local_layouts_case, check_against_oracle
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 40
 
-
-@pytest.mark.parametrize("seed", range(N_CASES))
+@pytest.mark.parametrize("seed", seed_range(40))
 def test_random_configuration(seed):
     w = random_workload(seed)
     inp = synthkv.make_inputs(w)
@@ -34,7 +32,7 @@ def test_random_configuration(seed):
                          reuse=True, log_name=f"fuzz{seed} reuse")
 
 
-@pytest.mark.parametrize("seed,lo,ln", layout_cases(20))
+@pytest.mark.parametrize("seed,lo,ln", layout_cases(layout_count(20)))
 def test_random_configuration_layouts(seed, lo, ln):
     w = random_workload(seed)
     _layouts_case(w, lo, ln, reuse=bool(seed % 2))

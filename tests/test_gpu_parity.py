@@ -25,7 +25,7 @@ from gpu_harness import (DeviceTables, RankPool, Workspace, log, rank_layers, sh
 
 pytestmark = pytest.mark.gpu
 
-from edgecases import EDGE, custom as _custom
+from edgecases import EDGE, SHIFTED_LAYOUTS, custom as _custom, shifted_old_lengths_case
 
 T = oracle.Topology
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -250,6 +250,49 @@ def test_mismatched_device_tables_are_contained():
     assert ws.flag() != 0
     for p in pairs:                        # nothing was copied
         assert torch.equal(staging[p], before[p])
+
+
+@pytest.mark.parametrize("lo,ln", SHIFTED_LAYOUTS)
+def test_local_copy_contains_shifted_device_lengths(lo, ln):
+    """Old device lengths that shift a sequence start (same total) give some rows of the local copies a
+    negative token index; those rows must be skipped and flagged, never read from before an old block.
+    (The CPU model of the kernels checks this case access by access: test_model_shifted_old_lengths.)"""
+    rk = _rk()
+    w, inp, (lens, offs, ids) = shifted_old_lengths_case()
+    L = w.num_layers
+    plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
+    old_host = hostpools.source_pools(w, inp.old_tables)
+    new_host = hostpools.sentinel_pools(w, inp.new_tables)
+    dto = DeviceTables(inp.old_tables)
+    dto.lens.copy_(torch.from_numpy(lens))
+    dto.ids.copy_(torch.from_numpy(ids))
+    dtn = DeviceTables(inp.new_tables)
+    ws = Workspace(plan)
+    W = plan.info.old_world
+    src = {r: _upload_layout(old_host[r], lo, rank_layers(r, w.old_topo, L), inp.old_tables.num_blocks)
+           for r in range(W)}
+    dst = {q: _upload_layout(new_host[q], ln, rank_layers(q, w.new_topo, L), inp.new_tables.num_blocks)
+           for q in range(W)}
+    flags = []
+    for r in range(W):
+        plan.copy_local(r, src[r][0], dto.dev, dst[r][0], dtn.host, dtn.dev, ws.buf, ws.bytes, stream_handle())
+        torch.cuda.synchronize()
+        flags.append(ws.flag())
+    assert all(f == 1 for f in flags), flags
+    nd = synthkv.numpy_dtype_for(w.elem_bytes)
+    for r in range(W):                    # sources untouched
+        for l, (kt, vt) in src[r][1].items():
+            want = oracle.encode_pool(old_host[r][l], lo)
+            assert np.array_equal(kt.cpu().numpy().view(nd), want[0])
+            assert np.array_equal(vt.cpu().numpy().view(nd), want[1])
+    live = np.zeros((inp.new_tables.num_blocks, inp.new_tables.block_size), bool)
+    for s_ in range(len(inp.lens)):
+        blk, slot = oracle.token_slots(inp.new_tables, s_)
+        live[blk, slot] = True
+    for q in range(W):                    # dead slots of the new pools untouched
+        for l, (kt, vt) in dst[q][1].items():
+            got = oracle.decode_pool([kt.cpu().numpy().view(nd), vt.cpu().numpy().view(nd)], ln)
+            assert np.array_equal(got[:, ~live], new_host[q][l][:, ~live]), f"rank {q} layer {l}: a dead slot written"
 
 
 # ---------------------------------------------------------------------------

@@ -17,8 +17,8 @@ import oracle
 import synthkv
 
 import kernel_model as km
-from edgecases import EDGE
-from fuzzcases import layout_cases, random_windows, random_workload
+from edgecases import EDGE, SHIFTED_LAYOUTS, shifted_old_lengths_case as _shifted_case
+from fuzzcases import layout_cases, layout_count, random_windows, random_workload, seed_range
 
 T = oracle.Topology
 
@@ -166,7 +166,7 @@ def test_model_layouts(lo, ln):
 # seeded random configurations (the GPU fuzz generator)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", seed_range(40))
 def test_model_fuzz(seed):
     w = random_workload(seed)
     inp = synthkv.make_inputs(w)
@@ -174,7 +174,7 @@ def test_model_fuzz(seed):
     check_model(w, inp, local=True, seed=seed)
 
 
-@pytest.mark.parametrize("seed,lo,ln", layout_cases(20))
+@pytest.mark.parametrize("seed,lo,ln", layout_cases(layout_count(20)))
 def test_model_fuzz_layouts(seed, lo, ln):
     w = random_workload(seed)
     inp = synthkv.make_inputs(w)
@@ -234,36 +234,14 @@ def test_model_full_size_layouts(lo, ln):
 # device tables that disagree with the host tables
 # ---------------------------------------------------------------------------
 
-def _shifted_case():
-    """Identity topology (every slice local) and old device tables whose lengths move 17 tokens from
-    sequence 1 to sequence 0 (same total, shifted starts), with sequence 1's first old block at physical
-    block 0: the first 16 rows of sequence 1 then get a negative token index in the local copies."""
-    from edgecases import custom
-    w = custom(num_layers=2, num_kv_heads=8, head_dim=64, old_topo=(2, 1), new_topo=(2, 1), num_seqs=3,
-               length_law=("fixed", 40), seed=5)
-    inp = synthkv.make_inputs(w)
-    t = inp.old_tables
-    lens = t.seq_lens.copy()
-    lens[0] += 17
-    lens[1] -= 17
-    ids = t.ids.copy()
-    first1 = int(t.offsets[1])
-    at0 = int(np.nonzero(ids == 0)[0][0]) if (ids == 0).any() else None
-    if at0 is None:
-        ids[first1] = 0
-    else:
-        ids[at0], ids[first1] = ids[first1], 0
-    return w, inp, (lens, t.offsets, ids)
-
-
-@pytest.mark.parametrize("lo,ln", [(0, 0), (1, 1), (2, 2), (0, 1)])
+@pytest.mark.parametrize("lo,ln", SHIFTED_LAYOUTS)
 def test_model_shifted_old_lengths_are_contained(lo, ln):
     """The local copies combine the new expansion's token offsets with the old one's; old device lengths
     that shift a sequence start (same total) must neither leave the pools nor go unreported."""
     w, inp, dev_old = _shifted_case()
     m = km.Migration(w, inp, lo, ln, data=True, dev_old=dev_old)
     flags = [m.copy_local(r) for r in range(min(m.old.tp * m.old.pp, m.new.tp * m.new.pp))]
-    assert any(flags), "shifted device lengths went unreported"
+    assert all(f == 1 for f in flags), f"shifted device lengths went unreported: {flags}"
 
 
 def test_model_out_of_range_ids_are_contained():

@@ -90,6 +90,12 @@ def parse():
     ap.add_argument("--ceiling", type=float, default=0.0, metavar="GIB",
                     help="only run the HBM access-pattern probes (libremp_probe.so) over buffers of this many GiB, "
                          "then exit")
+    ap.add_argument("--ceiling-shape", default=None, metavar="THREADS,UNROLL,CHUNKS",
+                    help="run the probes at this launch shape only (default: all 48)")
+    ap.add_argument("--ceiling-chunks", default="4096,8192",
+                    help="chunk sizes of the probes in bytes, comma separated")
+    ap.add_argument("--ceiling-window", type=float, default=0.0, metavar="MIB",
+                    help="draw the random chunk orders within consecutive windows of this many MiB (0: whole buffer)")
     return ap.parse_args()
 
 
@@ -304,10 +310,11 @@ def summarize_trace(path: str) -> int:
     return 0
 
 
-def ceiling(gib: float) -> int:
+def ceiling(args) -> int:
     """HBM access-pattern probes: 4 and 8 KiB chunks copied, read or written in address order or through a
-    random permutation, each at every launch shape, median of 3 launches; GB/s counts bytes read plus
-    bytes written."""
+    random permutation (optionally random only within windows of --ceiling-window MiB), each at every launch
+    shape (or --ceiling-shape), median of 3 launches; GB/s counts bytes read plus bytes written."""
+    gib = args.ceiling
     import ctypes
     import torch
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_18741_amd", "libremp_probe.so"))
@@ -318,37 +325,44 @@ def ceiling(gib: float) -> int:
                    ctypes.c_void_p]
     stream = torch.cuda.current_stream()
     shapes = [(t, u, c) for t in (256, 512, 1024) for u in (1, 2, 4, 8) for c in (1, 2, 4, 16)]
+    if args.ceiling_shape:
+        shapes = [tuple(int(x) for x in args.ceiling_shape.split(","))]
     patterns = [("copy, contiguous", 0, False, False), ("copy, random reads (gather)", 0, True, False),
                 ("copy, random writes (scatter)", 0, False, True), ("copy, random reads and writes", 0, True, True),
                 ("read only, contiguous", 1, False, False), ("read only, random", 1, True, False),
                 ("write only, contiguous", 2, False, False), ("write only, random", 2, False, True)]
     results = []
-    for chunk in (4096, 8192):
+    for chunk in [int(x) for x in args.ceiling_chunks.split(",")]:
         n = int(gib * (1 << 30)) // chunk
         src = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
         dst = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
         src.fill_(1)
         dst.fill_(2)
         g = torch.Generator(device="cpu").manual_seed(chunk)
-        perm_r = torch.randperm(n, generator=g).to(torch.int32).cuda()
-        perm_w = torch.randperm(n, generator=g).to(torch.int32).cuda()
+        win = max(1, int(args.ceiling_window * (1 << 20)) // chunk) if args.ceiling_window > 0 else n
+
+        def order():
+            """A random order of the n chunks, random only within consecutive windows of `win` chunks."""
+            parts = [a + torch.randperm(min(win, n - a), generator=g) for a in range(0, n, win)]
+            return torch.cat(parts).to(torch.int32).cuda()
+        perm_r, perm_w = order(), order()
         sink = torch.empty(1024 * 16, dtype=torch.uint8, device="cuda")
         for name, mode, rr, rw in patterns:
             moved = (2 if mode == 0 else 1) * n * chunk
             best = None
             for (t, u, c) in shapes:
-                args = (mode, src.data_ptr(), dst.data_ptr(), sink.data_ptr(), sink.numel(), n, chunk,
+                call = (mode, src.data_ptr(), dst.data_ptr(), sink.data_ptr(), sink.numel(), n, chunk,
                         perm_r.data_ptr() if rr else None, perm_w.data_ptr() if rw else None, t, u, c,
                         stream.cuda_stream)
                 if -(-n // c) * t >= (1 << 32):
                     continue                      # more work-items than one dispatch counts
-                if fn(*args) != 0:
+                if fn(*call) != 0:
                     raise RuntimeError(f"probe launch refused: {name} {t}x{u} cpw {c}")
                 ts = []
                 for _ in range(3):
                     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     e0.record()
-                    fn(*args)
+                    fn(*call)
                     e1.record()
                     e1.synchronize()
                     ts.append(e0.elapsed_time(e1))
@@ -362,7 +376,8 @@ def ceiling(gib: float) -> int:
         del src, dst, perm_r, perm_w, sink
         torch.cuda.empty_cache()
     print(json.dumps({"metric": "HBM access-pattern ceiling", "unit": "GB/s (read + write)", "buffer_GiB": gib,
-                      "shapes_tried": len(shapes), "results": results}))
+                      "random_window_MiB": args.ceiling_window or None, "shapes_tried": len(shapes),
+                      "results": results}))
     return 0
 
 
@@ -460,7 +475,7 @@ def main() -> int:
         copy_calibration(args.copy_calibration)
         return 0
     if args.ceiling > 0:
-        return ceiling(args.ceiling)
+        return ceiling(args)
     if args.library_calibration > 0:
         return library_calibration(args.library_calibration)
     if args.summarize_counters:
@@ -552,6 +567,7 @@ def main() -> int:
         sh.ws = tio.workspace(plan, dev)
         sh.stream = tio.current_stream()
         torch.cuda.synchronize()
+        log(f"pools and staging allocated and filled ({time.time() - t0:.1f}s)")
         sh.foreign_host = {}
         for (r, q) in pairs_in:
             if r == ro:
@@ -571,6 +587,7 @@ def main() -> int:
             plan.pack(r, arg, sh.dto.dev, tio.staging_args(bufs, r, W_new, as_src=True), sh.ws, sh.ws.numel(),
                       sh.stream)
             torch.cuda.synchronize()
+            log(f"staging of old rank {r} for new rank {q} packed ({time.time() - t0:.1f}s)")
             if tio.workspace_flag(sh.ws) != 0:
                 raise RuntimeError("device tables disagree with host tables")
             del tmp, arg, extra, bufs

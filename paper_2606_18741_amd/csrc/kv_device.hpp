@@ -26,7 +26,7 @@ struct BlockDesc {
 };
 
 // Values of the workspace status flag (int32 at byte 0 of the workspace).
-constexpr int32_t kFlagTables = 1;   // the device tables disagreed with the host tables
+constexpr int32_t kFlagTables = 1;   // the device tables would have indexed out of range
 constexpr int32_t kFlagStale = 2;    // a reusing call found descriptors of other tables
 
 // Check of reused descriptors.  A call that expands its own descriptors passes

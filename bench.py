@@ -96,6 +96,10 @@ def parse():
                     help="chunk sizes of the probes in bytes, comma separated")
     ap.add_argument("--ceiling-window", type=float, default=0.0, metavar="MIB",
                     help="draw the random chunk orders within consecutive windows of this many MiB (0: whole buffer)")
+    ap.add_argument("--phased", type=float, default=0.0, metavar="GIB",
+                    help="only run the phased-copy probe (a persistent copy whose workgroups wait for each other "
+                         "between loads and stores, so the chip reads and writes in separate phases) next to the "
+                         "plain contiguous chunk copy, over buffers of this many GiB, then exit")
     return ap.parse_args()
 
 
@@ -381,6 +385,73 @@ def ceiling(args) -> int:
     return 0
 
 
+def phased(args) -> int:
+    """Phased-copy probe: a contiguous copy by a persistent grid in batches of grid * threads * vecs 16-byte
+    vectors, with 0, 1 or 2 grid-wide waits per batch (between the loads and the stores; also after the
+    stores), next to the plain contiguous copy of 4 KiB chunks; median of 5 launches, GB/s counts bytes read
+    plus bytes written, time-outs are the waits that ended by their 200 us bound."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_18741_amd", "libremp_probe.so"))
+    chunks = lib.remp_probe_chunks
+    chunks.restype = ctypes.c_int32
+    chunks.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                       ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                       ctypes.c_int32, ctypes.c_void_p]
+    ph = lib.remp_probe_phased
+    ph.restype = ctypes.c_int32
+    ph.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_int32, ctypes.c_int32, ctypes.c_double, ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]
+    cap = int(args.phased * (1 << 30)) // (1 << 20) * (1 << 20)
+    src = torch.empty(cap, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(cap, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst.fill_(2)
+    sync = torch.zeros(2, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def rate(launch, moved):
+        if launch() != 0:
+            raise RuntimeError("probe launch refused")
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            launch()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return moved / statistics.median(ts) / 1e6
+
+    n = cap // 4096
+    plain = rate(lambda: chunks(0, src.data_ptr(), dst.data_ptr(), None, 0, n, 4096, None, None, 256, 1, 1, stream),
+                 2 * cap)
+    log(f"phased probe: plain copy of 4 KiB chunks (256 x 1): {plain:.1f} GB/s")
+    results = []
+    for t, v in ((256, 8), (512, 8), (1024, 8), (1024, 16)):
+        for b in (0, 1, 2):
+            res = ctypes.c_int32(0)
+            ph(None, None, None, 0, t, v, b, 0, 200.0, ctypes.byref(res), stream)   # refused: asks the resident limit
+            for grid in sorted({g for g in (256, res.value) if 0 < g <= res.value}):
+                batch = grid * t * v * 16
+                nbytes = cap // batch * batch
+                if nbytes == 0:
+                    continue
+                gbps = rate(lambda: ph(src.data_ptr(), dst.data_ptr(), sync.data_ptr(), nbytes, t, v, b, grid, 200.0,
+                                       None, stream), 2 * nbytes)
+                torch.cuda.synchronize()
+                timeouts = int(sync[1].item())
+                results.append({"threads": t, "vecs": v, "waits_per_batch": b, "grid": grid,
+                                "batch_MiB": batch >> 20, "GBps": round(gbps, 1), "timeouts_last_launch": timeouts})
+                log(f"phased probe: {t} x {v}, {b} waits per batch, grid {grid}, batch {batch >> 20} MiB: "
+                    f"{gbps:.1f} GB/s ({timeouts} waits timed out)")
+    if not torch.equal(dst[:1 << 20], src[:1 << 20]):
+        raise RuntimeError("phased copy did not copy")
+    print(json.dumps({"metric": "phased-copy probe", "unit": "GB/s (read + write)", "buffer_GiB": args.phased,
+                      "plain_4KiB_chunks_GBps": round(plain, 1), "results": results}))
+    return 0
+
+
 # KV workload -> the decoder whose weights the same switch rebuilds
 WEIGHT_MODELS = {"gqa70b": "LLAMA3_70B", "qwen30b": "QWEN3_30B_A3B", "ds32b": "QWEN2_32B"}
 
@@ -476,6 +547,8 @@ def main() -> int:
         return 0
     if args.ceiling > 0:
         return ceiling(args)
+    if args.phased > 0:
+        return phased(args)
     if args.library_calibration > 0:
         return library_calibration(args.library_calibration)
     if args.summarize_counters:

@@ -39,6 +39,28 @@ REMP_PROBE_API int32_t remp_probe_chunks(int32_t mode, const void* src, void* ds
                                          const int32_t* dst_idx, int32_t threads, int32_t unroll,
                                          int32_t chunks_per_wg, hipStream_t stream);
 
+/* Enqueue a phased copy of `bytes` from src to dst (device, 16-byte aligned,
+ * non-overlapping) on `stream`: a persistent grid of `grid` workgroups of
+ * `threads` lanes copies consecutive batches of grid * threads * vecs 16-byte
+ * vectors, each workgroup its own contiguous part of a batch, each lane `vecs`
+ * vectors held in registers between its loads and its stores.  barriers 0: no
+ * waits; 1: every workgroup waits, between the loads and the stores of each
+ * batch, until all workgroups have completed the batch's loads, so the chip
+ * reads and writes in separate phases; 2: also after the stores.  A wait ends
+ * after at most wait_us microseconds (then it is counted as a time-out), so the
+ * launch always completes; the waits never change the bytes copied.  sync: 8
+ * bytes of device memory; the call zeroes it first, and after the launch
+ * completes its second 32-bit word holds the number of timed-out waits.
+ * threads: 256, 512 or 1024; vecs: 4, 8 or 16; bytes a multiple of the batch;
+ * grid at most the number of workgroups the GPU holds at once, which is
+ * returned in *max_resident (if not NULL) whenever threads, vecs and barriers
+ * are valid, also when the call is refused (so a call with grid 0 queries it).
+ * Returns 0, -1 for an invalid argument (nothing enqueued), -2 for a HIP
+ * error. */
+REMP_PROBE_API int32_t remp_probe_phased(const void* src, void* dst, void* sync, int64_t bytes, int32_t threads,
+                                         int32_t vecs, int32_t barriers, int32_t grid, double wait_us,
+                                         int32_t* max_resident, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

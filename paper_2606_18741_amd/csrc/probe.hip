@@ -82,6 +82,106 @@ hipError_t launch_unroll(int32_t unroll, int32_t mode, dim3 grid, const char* sr
     }
 }
 
+// Grid-wide wait of the phased copy: every workgroup counts itself in at sync[0]
+// once all its lanes' memory operations have completed, then waits until
+// `target` arrivals are counted or `wait_ticks` of the constant-rate clock have
+// passed (then it counts a time-out in sync[1] and goes on).  Nothing depends on
+// the wait for correctness: each workgroup only moves its own vectors, so the
+// wait only lines up the phases of the workgroups, and the time bound ends it
+// even if some workgroups are not resident.
+__device__ __forceinline__ void grid_wait(uint32_t* sync, uint32_t target, uint64_t wait_ticks) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __hip_atomic_fetch_add(&sync[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t0 = static_cast<uint64_t>(wall_clock64());
+        while (__hip_atomic_load(&sync[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (static_cast<uint64_t>(wall_clock64()) - t0 > wait_ticks) {
+                __hip_atomic_fetch_add(&sync[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    __syncthreads();
+}
+
+// Phased copy: a persistent grid copies `cycles` consecutive batches of
+// gridDim.x * THREADS * VECS 16-byte vectors; in each batch workgroup w takes
+// its own contiguous THREADS * VECS vectors, each lane VECS of them held in
+// registers between its loads and its stores.  BARRIERS 0: no waits (the same
+// copy without phases); 1: a grid-wide wait between the loads and the stores of
+// every batch, so that the whole chip reads, then writes; 2: a second wait after
+// the stores.
+template <int THREADS, int VECS, int BARRIERS>
+__global__ __launch_bounds__(THREADS) void phased_copy(const V4* __restrict__ src, V4* __restrict__ dst,
+                                                       uint32_t* __restrict__ sync, int32_t cycles,
+                                                       uint64_t wait_ticks) {
+    const uint32_t g = gridDim.x;
+    uint32_t waits = 0;
+    for (int32_t c = 0; c < cycles; ++c) {
+        const uint64_t base = (static_cast<uint64_t>(c) * g + blockIdx.x) * (THREADS * VECS) + threadIdx.x;
+        V4 r[VECS];
+#pragma unroll
+        for (int j = 0; j < VECS; ++j) r[j] = __builtin_nontemporal_load(src + base + j * THREADS);
+        if (BARRIERS > 0) grid_wait(sync, ++waits * g, wait_ticks);
+#pragma unroll
+        for (int j = 0; j < VECS; ++j) __builtin_nontemporal_store(r[j], dst + base + j * THREADS);
+        if (BARRIERS > 1) grid_wait(sync, ++waits * g, wait_ticks);
+    }
+}
+
+__global__ void zero_words(uint32_t* p, int32_t n) {
+    if (static_cast<int32_t>(threadIdx.x) < n) p[threadIdx.x] = 0;
+}
+
+// Workgroups of phased_copy<THREADS, VECS, barriers> the GPU holds at once.
+template <int THREADS, int VECS>
+hipError_t resident_b(int32_t barriers, int32_t* out) {
+    const void* fn = barriers == 0   ? reinterpret_cast<const void*>(phased_copy<THREADS, VECS, 0>)
+                     : barriers == 1 ? reinterpret_cast<const void*>(phased_copy<THREADS, VECS, 1>)
+                                     : reinterpret_cast<const void*>(phased_copy<THREADS, VECS, 2>);
+    int per_cu = 0, dev = 0, cus = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, THREADS, 0);
+    if (e != hipSuccess) return e;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    *out = per_cu * cus;
+    return hipSuccess;
+}
+
+template <int THREADS>
+hipError_t resident_v(int32_t vecs, int32_t barriers, int32_t* out) {
+    switch (vecs) {
+        case 4: return resident_b<THREADS, 4>(barriers, out);
+        case 8: return resident_b<THREADS, 8>(barriers, out);
+        default: return resident_b<THREADS, 16>(barriers, out);
+    }
+}
+
+template <int THREADS, int VECS>
+hipError_t launch_phased_b(int32_t barriers, int32_t grid, const V4* src, V4* dst, uint32_t* sync, int32_t cycles,
+                           uint64_t ticks, hipStream_t s) {
+    hipLaunchKernelGGL(zero_words, dim3(1), dim3(64), 0, s, sync, 2);
+    if (barriers == 0)
+        hipLaunchKernelGGL((phased_copy<THREADS, VECS, 0>), dim3(grid), dim3(THREADS), 0, s, src, dst, sync, cycles, ticks);
+    else if (barriers == 1)
+        hipLaunchKernelGGL((phased_copy<THREADS, VECS, 1>), dim3(grid), dim3(THREADS), 0, s, src, dst, sync, cycles, ticks);
+    else
+        hipLaunchKernelGGL((phased_copy<THREADS, VECS, 2>), dim3(grid), dim3(THREADS), 0, s, src, dst, sync, cycles, ticks);
+    return hipGetLastError();
+}
+
+template <int THREADS>
+hipError_t launch_phased_v(int32_t vecs, int32_t barriers, int32_t grid, const V4* src, V4* dst, uint32_t* sync,
+                           int32_t cycles, uint64_t ticks, hipStream_t s) {
+    switch (vecs) {
+        case 4: return launch_phased_b<THREADS, 4>(barriers, grid, src, dst, sync, cycles, ticks, s);
+        case 8: return launch_phased_b<THREADS, 8>(barriers, grid, src, dst, sync, cycles, ticks, s);
+        default: return launch_phased_b<THREADS, 16>(barriers, grid, src, dst, sync, cycles, ticks, s);
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -112,6 +212,42 @@ int32_t remp_probe_chunks(int32_t mode, const void* src, void* dst, void* sink, 
     if (threads == 256) e = launch_unroll<256>(unroll, mode, g, s, d, k, n_chunks, cv, sh, src_idx, dst_idx, chunks_per_wg, stream);
     else if (threads == 512) e = launch_unroll<512>(unroll, mode, g, s, d, k, n_chunks, cv, sh, src_idx, dst_idx, chunks_per_wg, stream);
     else e = launch_unroll<1024>(unroll, mode, g, s, d, k, n_chunks, cv, sh, src_idx, dst_idx, chunks_per_wg, stream);
+    return e == hipSuccess ? 0 : -2;
+}
+
+int32_t remp_probe_phased(const void* src, void* dst, void* sync, int64_t bytes, int32_t threads, int32_t vecs,
+                          int32_t barriers, int32_t grid, double wait_us, int32_t* max_resident, hipStream_t stream) {
+    int32_t resident = 0;
+    if (max_resident) *max_resident = 0;
+    if (threads != 256 && threads != 512 && threads != 1024) return -1;
+    if (vecs != 4 && vecs != 8 && vecs != 16) return -1;
+    if (barriers < 0 || barriers > 2) return -1;
+    const hipError_t re = threads == 256   ? resident_v<256>(vecs, barriers, &resident)
+                          : threads == 512 ? resident_v<512>(vecs, barriers, &resident)
+                                           : resident_v<1024>(vecs, barriers, &resident);
+    if (re != hipSuccess) return -2;
+    if (max_resident) *max_resident = resident;
+    if (!src || !dst || !sync || bytes <= 0 || grid < 1 || grid > resident) return -1;
+    if (!(wait_us > 0.0) || wait_us > 1.0e6) return -1;
+    if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 16 || reinterpret_cast<uintptr_t>(sync) % 4)
+        return -1;
+    const int64_t batch = static_cast<int64_t>(grid) * threads * vecs * 16;
+    if (bytes % batch) return -1;
+    const int64_t cycles = bytes / batch;
+    if (cycles * 2 * grid >= (int64_t(1) << 31)) return -1;
+    int dev = 0, khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+        khz <= 0)
+        return -2;
+    const uint64_t ticks = static_cast<uint64_t>(wait_us * khz / 1000.0) + 1;
+    const V4* s = static_cast<const V4*>(src);
+    V4* d = static_cast<V4*>(dst);
+    uint32_t* y = static_cast<uint32_t*>(sync);
+    const int32_t cyc = static_cast<int32_t>(cycles);
+    hipError_t e;
+    if (threads == 256) e = launch_phased_v<256>(vecs, barriers, grid, s, d, y, cyc, ticks, stream);
+    else if (threads == 512) e = launch_phased_v<512>(vecs, barriers, grid, s, d, y, cyc, ticks, stream);
+    else e = launch_phased_v<1024>(vecs, barriers, grid, s, d, y, cyc, ticks, stream);
     return e == hipSuccess ? 0 : -2;
 }
 

@@ -63,13 +63,13 @@ def test_exports_every_declared_symbol():
 
 
 def test_probe_library_exports_and_refuses_bad_arguments():
-    """libremp_probe.so (HBM access-pattern probes, measurement only) exports its one entry point and refuses
+    """libremp_probe.so (HBM access-pattern probes, measurement only) exports its two entry points and refuses
     invalid arguments before touching the GPU."""
     import ctypes
     import subprocess
     path = os.path.join(os.path.dirname(rk._lib._LIB_PATH), "libremp_probe.so")
     out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True).stdout
-    assert {ln.split()[-1] for ln in out.splitlines() if "remp_" in ln} == {"remp_probe_chunks"}
+    assert {ln.split()[-1] for ln in out.splitlines() if "remp_" in ln} == {"remp_probe_chunks", "remp_probe_phased"}
     fn = ctypes.CDLL(path).remp_probe_chunks
     fn.restype = ctypes.c_int32
     fn.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
@@ -80,6 +80,17 @@ def test_probe_library_exports_and_refuses_bad_arguments():
         a = list(ok)
         a[i] = bad
         assert fn(*a) == -1, (i, bad)
+    ph = ctypes.CDLL(path).remp_probe_phased
+    ph.restype = ctypes.c_int32
+    ph.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_int32, ctypes.c_int32, ctypes.c_double, ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]
+    resident = ctypes.c_int32(-1)
+    ok = [1 << 40, 1 << 41, 1 << 42, 1 << 30, 256, 8, 1, 256, 200.0, ctypes.byref(resident), None]
+    for i, bad in ((4, 128), (5, 3), (6, 3), (6, -1)):   # refused before any HIP call
+        a = list(ok)
+        a[i] = bad
+        assert ph(*a) == -1, (i, bad)
+        assert resident.value == 0
 
 
 def test_only_the_abi_is_exported_from_host_code():

@@ -389,7 +389,8 @@ def phased(args) -> int:
     """Phased-copy probe: a contiguous copy by a persistent grid in batches of grid * threads * vecs 16-byte
     vectors, with 0, 1 or 2 grid-wide waits per batch (between the loads and the stores; also after the
     stores), next to the plain contiguous copy of 4 KiB chunks; median of 5 launches, GB/s counts bytes read
-    plus bytes written, time-outs are the waits that ended by their 200 us bound."""
+    plus bytes written, time-outs are the waits that ended by their 200 us bound.  Each shape's first launch
+    is checked byte for byte against the source."""
     import ctypes
     import torch
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_18741_amd", "libremp_probe.so"))
@@ -403,16 +404,20 @@ def phased(args) -> int:
     ph.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                    ctypes.c_int32, ctypes.c_int32, ctypes.c_double, ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]
     cap = int(args.phased * (1 << 30)) // (1 << 20) * (1 << 20)
-    src = torch.empty(cap, dtype=torch.uint8, device="cuda")
+    src = torch.randint(0, 256, (cap,), dtype=torch.uint8, device="cuda",
+                        generator=torch.Generator(device="cuda").manual_seed(7))
     dst = torch.empty(cap, dtype=torch.uint8, device="cuda")
-    src.fill_(1)
-    dst.fill_(2)
     sync = torch.zeros(2, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream().cuda_stream
 
     def rate(launch, moved):
+        """GB/s of `launch` (moving `moved` bytes), after a first launch into a cleared dst is checked
+        byte for byte over the moved range."""
+        dst.zero_()
         if launch() != 0:
             raise RuntimeError("probe launch refused")
+        if not torch.equal(dst[:moved // 2], src[:moved // 2]):
+            raise RuntimeError("probe copy differs from its source")
         ts = []
         for _ in range(5):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -445,8 +450,6 @@ def phased(args) -> int:
                                 "batch_MiB": batch >> 20, "GBps": round(gbps, 1), "timeouts_last_launch": timeouts})
                 log(f"phased probe: {t} x {v}, {b} waits per batch, grid {grid}, batch {batch >> 20} MiB: "
                     f"{gbps:.1f} GB/s ({timeouts} waits timed out)")
-    if not torch.equal(dst[:1 << 20], src[:1 << 20]):
-        raise RuntimeError("phased copy did not copy")
     print(json.dumps({"metric": "phased-copy probe", "unit": "GB/s (read + write)", "buffer_GiB": args.phased,
                       "plain_4KiB_chunks_GBps": round(plain, 1), "results": results}))
     return 0

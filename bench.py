@@ -317,7 +317,8 @@ def summarize_trace(path: str) -> int:
 def ceiling(args) -> int:
     """HBM access-pattern probes: 4 and 8 KiB chunks copied, read or written in address order or through a
     random permutation (optionally random only within windows of --ceiling-window MiB), each at every launch
-    shape (or --ceiling-shape), median of 3 launches; GB/s counts bytes read plus bytes written."""
+    shape (or --ceiling-shape), median of 3 launches; GB/s counts bytes read plus bytes written.  The copy
+    patterns are rerun at their best shape into a cleared destination and checked chunk by chunk."""
     gib = args.ceiling
     import ctypes
     import torch
@@ -338,10 +339,9 @@ def ceiling(args) -> int:
     results = []
     for chunk in [int(x) for x in args.ceiling_chunks.split(",")]:
         n = int(gib * (1 << 30)) // chunk
-        src = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
+        src = torch.randint(0, 256, (n * chunk,), dtype=torch.uint8, device="cuda",
+                            generator=torch.Generator(device="cuda").manual_seed(chunk))
         dst = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
-        src.fill_(1)
-        dst.fill_(2)
         g = torch.Generator(device="cpu").manual_seed(chunk)
         win = max(1, int(args.ceiling_window * (1 << 20)) // chunk) if args.ceiling_window > 0 else n
 
@@ -373,6 +373,19 @@ def ceiling(args) -> int:
                 gbps = moved / statistics.median(ts) / 1e6
                 if best is None or gbps > best[0]:
                     best = (gbps, t, u, c)
+            if mode == 0:
+                # the best shape once more into a cleared destination: chunk dst_idx[i] must hold chunk src_idx[i]
+                dst.zero_()
+                fn(mode, src.data_ptr(), dst.data_ptr(), sink.data_ptr(), sink.numel(), n, chunk,
+                   perm_r.data_ptr() if rr else None, perm_w.data_ptr() if rw else None, best[1], best[2], best[3],
+                   stream.cuda_stream)
+                sv, dv = src.view(n, chunk), dst.view(n, chunk)
+                for lo in range(0, n, 1 << 18):
+                    hi = min(n, lo + (1 << 18))
+                    si = perm_r[lo:hi].long() if rr else torch.arange(lo, hi, device="cuda")
+                    di = perm_w[lo:hi].long() if rw else torch.arange(lo, hi, device="cuda")
+                    if not torch.equal(dv[di], sv[si]):
+                        raise RuntimeError(f"probe copy differs from its source: {chunk} B {name}")
             results.append({"chunk_bytes": chunk, "pattern": name, "GBps": round(best[0], 1),
                             "frac_of_peak": round(best[0] / PEAK_HBM_GBS, 4),
                             "best_shape": {"threads": best[1], "unroll": best[2], "chunks_per_workgroup": best[3]}})

@@ -55,6 +55,14 @@ EDGE = {
 }
 
 
+# The library's size limits: 2^31 - 2^20 live tokens (the plan takes at most 2^31 - 1) in 2048 sequences,
+# re-blocked from 16 to 8 tokens per block, so the new tables hold 2^28 - 2^17 live blocks (the plan takes
+# fewer than 2^28).  One 4-byte head row per token keeps each K or V pool at 8 GiB; one rank keeps everything.
+LIMITS = custom(name="limits", num_layers=1, num_kv_heads=1, head_dim=4, elem_bytes=1, dtype="u8",
+                old_block_size=16, new_block_size=8, num_seqs=2048, length_law=("fixed", (1 << 20) - (1 << 9)),
+                pool_law=("slack", 1.001), old_topo=(1, 1), new_topo=(1, 1), role=(0, 0), seed=31)
+
+
 # Pool layout pairs (old, new) of the shifted-lengths case: NHD, HND and ROCm tiles, same and mixed.
 SHIFTED_LAYOUTS = [(0, 0), (1, 1), (2, 2), (0, 1)]
 

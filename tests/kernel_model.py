@@ -50,6 +50,7 @@ TILE_WG_BYTES = 16 * 1024
 DESCS_PER_BUCKET = 4
 NHD, HND, ROCM = 0, 1, 2
 INT32_MAX = 2 ** 31 - 1
+EMIT_CHUNK = 1 << 23          # expand_emit lanes modelled at once
 
 # (threads, loads per lane, XCD cell order) of each launch kind
 PACK_SMALL = (64, 4, False)
@@ -180,21 +181,30 @@ class Mem:
                              f"({reg.size} bytes)")
         return k, off
 
+    # accesses of one call are modelled in chunks of this many lanes, to bound the temporaries
+    CHUNK = 1 << 20
+
     def load(self, addrs, n: int, what: str) -> np.ndarray:
         addrs = np.asarray(addrs, dtype=np.int64).reshape(-1)
         out = np.zeros((addrs.size, n), np.uint8)
-        if addrs.size == 0:
-            return out
-        k, off = self._locate(addrs, n, what)
-        for ri in np.unique(k):
-            m = k == ri
-            reg = self.regions[int(ri)]
-            if reg.data is not None:
-                out[m] = reg.data[off[m][:, None] + np.arange(n)]
+        for a in range(0, addrs.size, self.CHUNK):
+            part = addrs[a:a + self.CHUNK]
+            k, off = self._locate(part, n, what)
+            for ri in np.unique(k):
+                m = k == ri
+                reg = self.regions[int(ri)]
+                if reg.data is not None:
+                    out[a:a + self.CHUNK][m] = reg.data[off[m][:, None] + np.arange(n)]
         return out
 
     def store(self, addrs, vals: np.ndarray, what: str) -> None:
+        """Stores of one call; a byte stored twice (by two lanes, or by this call and an earlier one since
+        the last reset_writes) is an error."""
         addrs = np.asarray(addrs, dtype=np.int64).reshape(-1)
+        for a in range(0, addrs.size, self.CHUNK):
+            self._store(addrs[a:a + self.CHUNK], vals[a:a + self.CHUNK], what)
+
+    def _store(self, addrs: np.ndarray, vals: np.ndarray, what: str) -> None:
         if addrs.size == 0:
             return
         n = vals.shape[1]
@@ -276,9 +286,10 @@ def expand(mem: Mem, tables: Tables, S: int, bs: int, nnz: int, num_blocks: int,
     mem.store_i32(scan_addr, np.arange(S + 1), tok_off, "expand_scan: token offsets")
     mem.store_i32(scan_addr + 4 * (S + 1), np.arange(S + 1), blk_off, "expand_scan: block offsets")
 
-    desc = np.zeros((n_desc, 4), np.int64)
-    if n_desc:
-        b = np.arange(n_desc, dtype=np.int64)
+    # (block, tok, n, seq) per descriptor; every field of a descriptor the kernel emits fits int32
+    desc = np.zeros((n_desc, 4), np.int32)
+    for c0 in range(0, n_desc, EMIT_CHUNK):     # lanes in chunks, to bound the temporaries
+        b = np.arange(c0, min(n_desc, c0 + EMIT_CHUNK), dtype=np.int64)
         # last s in [0, S] with blk_off[s] <= b (binary search over the block offsets the scan wrote)
         lo = np.searchsorted(blk_off, b, side="right") - 1
         lo = np.clip(lo, 0, S)
@@ -286,24 +297,29 @@ def expand(mem: Mem, tables: Tables, S: int, bs: int, nnz: int, num_blocks: int,
         ok = lo < S
         s = np.where(ok, lo, 0)
         j = b - blk_off[s]
-        nn = np.zeros(n_desc, np.int64)
-        r = np.zeros(n_desc, np.int64)
+        nn = np.zeros(b.size, np.int64)
+        r = np.zeros(b.size, np.int64)
         if ok.any():
             nn[ok] = mem.load_i32(tables.lens, s[ok], "expand_emit: seq_lens")
             r[ok] = mem.load_i32(tables.offs, s[ok], "expand_emit: row_offsets") + j[ok]
         ok &= (r >= 0) & (r < nnz)
-        ids = np.zeros(n_desc, np.int64)
+        ids = np.zeros(b.size, np.int64)
         if ok.any():
             ids[ok] = mem.load_i32(tables.ids, r[ok], "expand_emit: block_ids")
         t0 = tok_off[s] + j * bs
         cnt = np.minimum(nn - j * bs, bs)
         ok &= (ids >= 0) & (ids < num_blocks) & (cnt > 0) & (t0 >= 0) & (t0 + cnt <= total_tokens)
-        desc[ok] = np.stack([ids[ok], t0[ok], cnt[ok], s[ok]], axis=1)
+        part = np.zeros((b.size, 4), np.int64)
+        part[ok] = np.stack([ids[ok], t0[ok], cnt[ok], s[ok]], axis=1)
+        if (part > INT32_MAX).any() or (part < 0).any():
+            raise ModelError("expand_emit: a descriptor field leaves int32")
+        desc[b[0]:b[-1] + 1] = part
         if not ok.all():
             flag = 1
-        mem.store(desc_addr + 16 * b, desc.astype(np.int32).view(np.uint8).reshape(-1, 16), "expand_emit: descriptors")
+        mem.store(desc_addr + 16 * b, desc[b[0]:b[-1] + 1].view(np.uint8).reshape(-1, 16),
+                  "expand_emit: descriptors")
         if bucket_addr is not None:
-            bk = bucket_of(desc[:, 0], num_blocks if num_blocks > 0 else 1, nb)
+            bk = bucket_of(part[:, 0], num_blocks if num_blocks > 0 else 1, nb)
             mem.load_i32(bucket_addr, np.unique(bk), "expand_emit: bucket count")
     return Expanded(desc, tok_off, blk_off, flag)
 
@@ -329,16 +345,22 @@ def sort_new(mem: Mem, desc: np.ndarray, num_blocks: int, bucket_addr: int, sort
     cnt = np.bincount(bk, minlength=nb)
     cursor = np.concatenate([[0], np.cumsum(cnt)[:-1]])
     mem.store_i32(bucket_addr, np.arange(nb), np.zeros(nb), "sort_scan: counters")   # rewritten in place
-    out = np.zeros_like(desc)
+    # the lanes' atomic increments arrive in a random order; lane i takes its bucket's cursor and advances it,
+    # so within a bucket positions follow the arrival order: a stable sort of the arrival order by bucket
+    arrival = rng.permutation(n)
+    order = arrival[np.argsort(bk[arrival], kind="stable")]
+    del arrival
     pos = np.empty(n, np.int64)
-    for i in rng.permutation(n):
-        pos[i] = cursor[bk[i]]
-        cursor[bk[i]] += 1
-    if not ((pos >= 0) & (pos < n)).all() or np.unique(pos).size != n:
+    pos[order] = np.arange(n, dtype=np.int64)
+    del order
+    if not ((pos >= 0) & (pos < n)).all() or (np.bincount(pos, minlength=n) != 1).any():
         raise ModelError("sort_scatter positions are not a permutation")
+    if ((pos < cursor[bk]) | (pos >= cursor[bk] + cnt[bk])).any():
+        raise ModelError("sort_scatter position outside its bucket's range")
+    out = np.zeros_like(desc)
     out[pos] = desc
-    mem.store(sorted_addr + 16 * pos, desc.astype(np.int32).view(np.uint8).reshape(-1, 16),
-              "sort_scatter: sorted descriptors")
+    d = np.ascontiguousarray(desc, dtype=np.int32)
+    mem.store(sorted_addr + 16 * pos, d.view(np.uint8).reshape(-1, 16), "sort_scatter: sorted descriptors")
     return out
 
 

@@ -10,6 +10,8 @@ local copy without its negative-token check) must be caught.
 """
 from __future__ import annotations
 
+import os
+
 import numpy as np
 import pytest
 
@@ -17,7 +19,7 @@ import oracle
 import synthkv
 
 import kernel_model as km
-from edgecases import EDGE, SHIFTED_LAYOUTS, shifted_old_lengths_case as _shifted_case
+from edgecases import EDGE, LIMITS, SHIFTED_LAYOUTS, shifted_old_lengths_case as _shifted_case
 from fuzzcases import layout_cases, layout_count, random_windows, random_workload, seed_range
 
 T = oracle.Topology
@@ -219,6 +221,20 @@ def test_model_full_size_launch_shapes(name):
         for Lc in m.local_launches(ro, 0, w.num_layers):
             _coverage(Lc, m.n_new)
         assert m.copy_local(ro, sample=48) == 0
+
+
+@pytest.mark.skipif(not os.environ.get("REMP_MODEL_LIMITS"),
+                    reason="about 25 minutes and 40 GiB of host memory: set REMP_MODEL_LIMITS=1")
+def test_model_size_limits():
+    """The size-limit case of the GPU suite (2^31 - 2^20 tokens, 2^28 - 2^17 new live blocks): the whole
+    expansion and descriptor sort of both sides, then sampled workgroups of every pack, unpack and local-copy
+    launch, bounds and exactly-once writes checked."""
+    w = LIMITS
+    m = km.Migration(w, synthkv.make_inputs(w), data=False, seed=3)
+    assert m.T == (1 << 31) - (1 << 20) and m.n_new == (1 << 28) - (1 << 17)
+    assert m.pack(0, sample=64) == 0
+    assert m.unpack(0, sample=64) == 0
+    assert m.copy_local(0, sample=64) == 0
 
 
 @pytest.mark.parametrize("lo,ln", [(1, 1), (2, 2), (0, 2), (1, 0)])

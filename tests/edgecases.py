@@ -48,6 +48,14 @@ EDGE = {
                                       new_topo=(4, 1), old_block_size=16, new_block_size=32),
     "short_row_shares_fp8": custom(num_layers=4, num_kv_heads=32, head_dim=128, elem_bytes=1,
                                    old_topo=(8, 1), new_topo=(2, 2), old_block_size=16, new_block_size=32),
+    # large blocks (128 -> 256 tokens: 128-512 KiB units, more than a workgroup's byte target)
+    "large_blocks_reblock": custom(num_layers=2, num_kv_heads=8, head_dim=128, old_block_size=128,
+                                   new_block_size=256, old_topo=(2, 1), new_topo=(1, 2),
+                                   length_law=("uniform", 0, 2000)),
+    # one KV head of 576 elements at every tensor rank (a compressed latent cache, replicated by
+    # tensor parallelism): the extreme of replication, 1152-byte rows
+    "replicated_single_latent_head": custom(num_layers=4, num_kv_heads=1, head_dim=576, old_topo=(4, 1),
+                                           new_topo=(2, 2)),
     # explicit uneven pipeline partitions
     "uneven_pp": custom(num_layers=5, old_topo=(2, 2, (0, 3, 5)), new_topo=(1, 3, (0, 1, 2, 5))),
     "uneven_to_even": custom(num_layers=6, old_topo=(1, 4, (0, 1, 3, 4, 6)), new_topo=(2, 2),

@@ -14,6 +14,10 @@ if TESTS not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: full-size workload run")
+    if os.environ.get("PYTEST_XDIST_WORKER"):
+        # several test processes share the cores: one intra-op thread each, or they oversubscribe them
+        import torch
+        torch.set_num_threads(1)
 
 
 def pytest_collection_modifyitems(config, items):

@@ -299,6 +299,8 @@ REMP_API remp_status remp_kv_unpack(const remp_kv_plan_t* plan, int32_t new_rank
  * status: NULL, or a 4-byte aligned device int32 that receives the status
  * flag remp_kv_workspace_bytes describes (0, 1 or 2); with NULL the flag stays
  * in the static array.
+ * stream: NULL or a stream of the current device, whose copy of the array the
+ * call uses; a stream of another device is refused (REMP_E_INVALID).
  * Every call on one device shares that device's array and finds the contents
  * the last call left: REMP_KV_REUSE_DESCRIPTORS reuses the descriptors of the
  * last expanding call on the device when their stamps match (flag 2

@@ -846,9 +846,16 @@ constexpr int kMaxScratchDevices = 64;
 static std::atomic<char*> g_scratch_ptr[kMaxScratchDevices];
 static std::mutex g_scratch_mu;
 
-static remp_status scratch_of_current_device(char** out) {
+static remp_status scratch_of_current_device(hipStream_t stream, char** out) {
     int dev = -1;
     if (remp_status st = hip_check(hipGetDevice(&dev), "hipGetDevice")) return st;
+    if (stream) {   // the kernels run on the stream's device: its scratch must be that device's copy
+        hipDevice_t sdev = -1;
+        if (remp_status st = hip_check(hipStreamGetDevice(stream, &sdev), "hipStreamGetDevice")) return st;
+        if (sdev != dev)
+            return fail(REMP_E_INVALID, "the stream belongs to device " + std::to_string(sdev) +
+                                            ", the current device is " + std::to_string(dev));
+    }
     if (dev < 0 || dev >= kMaxScratchDevices)
         return fail(REMP_E_UNSUPPORTED, "device index " + std::to_string(dev) + " beyond the static scratch table");
     char* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
@@ -965,7 +972,7 @@ remp_status remp_kv_unpack_noalloc(const remp_kv_plan_t* plan, int32_t new_rank,
     if (status && !aligned(status, 4)) return fail(REMP_E_ALIGN, "status is not 4-byte aligned");
     if (remp_status st = check_unpack_args(plan, new_rank, layer_begin, layer_end, staging, dst, flags)) return st;
     char* ws = nullptr;
-    if (remp_status st = scratch_of_current_device(&ws)) return st;
+    if (remp_status st = scratch_of_current_device(stream, &ws)) return st;
     return unpack_impl(plan, new_rank, layer_begin, layer_end, staging, dst, new_tables, new_dev_tables, ws,
                        status ? status : reinterpret_cast<int32_t*>(ws), flags, stream);
 }

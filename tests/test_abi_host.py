@@ -93,6 +93,29 @@ def test_probe_library_exports_and_refuses_bad_arguments():
         assert resident.value == 0
 
 
+def test_noalloc_refusals_before_any_device_call():
+    """remp_kv_unpack_noalloc validates before it touches a device: a plan whose workspace exceeds the static
+    scratch (REMP_E_SIZE), a misaligned status word (REMP_E_ALIGN) and a rank outside the new topology
+    (REMP_E_RANGE) are refused on a machine without a GPU."""
+    n = 1 << 22                                     # one sequence, 262144 blocks of 16 tokens
+    big = rk.HostTables(np.array([n], np.int32), np.array([0, n // 16], np.int32),
+                        np.arange(n // 16, dtype=np.int32), n // 16)
+    plan = rk.Plan((1, 1), (1, 1), (1, 1, 8, 2, 16, 16), big)
+    assert plan.workspace_bytes > 8 << 20           # REMP_KV_NOALLOC_SCRATCH_BYTES
+    none_pool = lambda nb: rk.PoolArg([None], [None], nb)
+    with pytest.raises(rk.RempError) as e:
+        plan.unpack_noalloc(0, rk.buffers([None]), none_pool(n // 16), big, rk.dev_tables(None, None, None), None, 0)
+    assert e.value.status_name == "REMP_E_SIZE"
+    small = rk.HostTables(np.array([37], np.int32), np.array([0, 3], np.int32), np.array([5, 0, 2], np.int32), 8)
+    plan = rk.Plan((1, 1), (1, 1), (1, 1, 8, 2, 16, 16), small)
+    with pytest.raises(rk.RempError) as e:
+        plan.unpack_noalloc(0, rk.buffers([None]), none_pool(8), small, rk.dev_tables(None, None, None), 0x1002, 0)
+    assert e.value.status_name == "REMP_E_ALIGN"
+    with pytest.raises(rk.RempError) as e:
+        plan.unpack_noalloc(1, rk.buffers([None]), none_pool(8), small, rk.dev_tables(None, None, None), None, 0)
+    assert e.value.status_name == "REMP_E_RANGE"
+
+
 def test_only_the_abi_is_exported_from_host_code():
     import subprocess
     out = subprocess.run(["nm", "-D", "--defined-only", rk._lib._LIB_PATH], capture_output=True, text=True).stdout

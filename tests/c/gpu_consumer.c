@@ -231,6 +231,60 @@ int main(int argc, char** argv) {
     printf("workspace flag %d\n", flag);
     if (flag != 0) FAIL("workspace flag %d after the migration", flag);
 
+    /* the allocation-free unpack, whole cache in one call per new rank, into fresh copies of the new pools
+       (the same starting bytes): every byte equal to what remp_kv_unpack wrote above */
+    int noalloc_ranks = 0;
+    if (ws_bytes <= REMP_KV_NOALLOC_SCRATCH_BYTES) {
+        int32_t* d_status;
+        HIP(hipMalloc((void**)&d_status, 4));
+        HIP(hipMemset(d_status, 0x7F, 4));
+        for (int32_t q = 0; q < Wn; ++q) {
+            int32_t first, count;
+            rank_layers(q, tpn, ppn, L, &first, &count);
+            if (count == 0) continue;
+            void** mem2 = (void**)calloc((size_t)count, sizeof(void*));
+            void** k2 = (void**)calloc((size_t)count, sizeof(void*));
+            void** v2 = (void**)calloc((size_t)count, sizeof(void*));
+            for (int32_t i = 0; i < count; ++i) {
+                char name[256];
+                snprintf(name, sizeof(name), "new_%d_%d.bin", q, first + i);
+                void* host = read_file(name, 2 * new_kv);
+                HIP(hipMalloc(&mem2[i], 2 * new_kv));
+                HIP(hipMemcpy(mem2[i], host, 2 * new_kv, hipMemcpyHostToDevice));
+                free(host);
+                k2[i] = mem2[i];
+                v2[i] = (char*)mem2[i] + new_kv;
+            }
+            remp_kv_pool pool2 = new_pool[q];
+            pool2.k = k2;
+            pool2.v = v2;
+            for (int32_t r = 0; r < Wo; ++r) {
+                const size_t pq = (size_t)r * Wn + q;
+                out[r].ptr = stage[pq];
+                out[r].bytes = stage[pq] ? stage_bytes[pq] : 0;
+            }
+            REMP(remp_kv_unpack_noalloc(plan, q, 0, L, out, &pool2, &new_tables, &dev_new, d_status, 0u, stream));
+            HIP(hipStreamSynchronize(stream));
+            int32_t status = -1;
+            HIP(hipMemcpy(&status, d_status, 4, hipMemcpyDeviceToHost));
+            if (status != 0) FAIL("no-alloc unpack of rank %d: status %d", q, status);
+            void* a_host = malloc(2 * new_kv);
+            void* b_host = malloc(2 * new_kv);
+            if (!a_host || !b_host) FAIL("out of host memory");
+            for (int32_t i = 0; i < count; ++i) {
+                HIP(hipMemcpy(a_host, new_mem[(size_t)q * L + i], 2 * new_kv, hipMemcpyDeviceToHost));
+                HIP(hipMemcpy(b_host, mem2[i], 2 * new_kv, hipMemcpyDeviceToHost));
+                if (memcmp(a_host, b_host, 2 * new_kv) != 0)
+                    FAIL("no-alloc unpack of rank %d, layer %d differs from remp_kv_unpack", q, first + i);
+                HIP(hipFree(mem2[i]));
+            }
+            free(a_host), free(b_host), free(mem2), free(k2), free(v2);
+            ++noalloc_ranks;
+        }
+        HIP(hipFree(d_status));
+    }
+    printf("no-alloc unpack equal to remp_kv_unpack on %d ranks\n", noalloc_ranks);
+
     /* results */
     for (int32_t q = 0; q < Wn; ++q) {
         int32_t first, count;

@@ -6,7 +6,10 @@ every new rank's unpack through include/remp_kv.h in two layer windows, the
 calls after the first reusing the block descriptors.  No Python or torch runs
 in that process.  This test writes its inputs (seeded tables and pools),
 compiles and runs it, and compares every byte of every new pool and staging
-buffer it returns with the oracle.
+buffer it returns with the oracle.  The program then runs the allocation-free
+unpack (remp_kv_unpack_noalloc) of every new rank over the whole cache into
+fresh copies of the new pools and checks them byte for byte against what
+remp_kv_unpack wrote.
 """
 from __future__ import annotations
 
@@ -87,6 +90,8 @@ def test_c_program_migration_matches_oracle(name, tmp_path):
     print(run.stdout, run.stderr, flush=True)
     assert run.returncode == 0, run.stdout + run.stderr
     assert "workspace flag 0" in run.stdout
+    noalloc = [ln for ln in run.stdout.splitlines() if ln.startswith("no-alloc unpack equal")]
+    assert noalloc and int(noalloc[0].split(" on ")[1].split()[0]) > 0, run.stdout
 
     plan = rk.Plan(w.old_topo, w.new_topo, (L, H, w.head_dim, w.elem_bytes, w.old_block_size, w.new_block_size),
                    rk.HostTables.of(inp.old_tables))

@@ -4,8 +4,9 @@ remp_kv_unpack_noalloc keeps its scan, descriptor and sort areas in a static
 device array of the library instead of a caller workspace.  Its new pools must
 equal, byte for byte, what remp_kv_unpack writes from the same staging (and the
 oracle's pools), on consecutive calls whose inputs differ in size, with the
-status flag delivered to a caller int32 or kept in the array, and with
-descriptor reuse accepted only for the tables the array last expanded.
+status flag delivered to a caller int32 or kept in the array, with
+descriptor reuse accepted only for the tables the array last expanded, and
+when captured into a HIP graph and replayed.
 """
 from __future__ import annotations
 
@@ -142,3 +143,44 @@ def test_noalloc_refuses_plans_beyond_the_scratch():
         plan.unpack_noalloc(0, rk.buffers([None]), rk.PoolArg([None], [None], n // 16), tables,
                             rk.dev_tables(None, None, None), None, 0)
     assert e.value.status_name == "REMP_E_SIZE"
+
+
+@pytest.mark.gpu
+def test_noalloc_under_graph_capture():
+    """The use the entry point exists for: a no-alloc unpack captured into a HIP graph (after a first call
+    outside the capture resolved the device's array) and replayed three times.  Before every replay the
+    destination is reset to its sentinel bytes and another plan's no-alloc unpack runs eagerly, overwriting
+    the static array; every replay must expand the tables again and equal the oracle, status 0."""
+    torch = _torch()
+    case = _Case(synthkv.reduced(synthkv.GQA_70B, num_seqs=5, max_len=300))
+    other = _Case(synthkv.reduced(synthkv.MHA_7B, num_seqs=2, max_len=80))
+    q = 0
+    dst = case._pool(q)
+    fresh = case._pool(q)
+    st = _status(9)
+
+    def run(stream):
+        case.plan.unpack_noalloc(q, case._args(q), dst.arg, case.dtn.host, case.dtn.dev, st, stream)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run(side.cuda_stream)                       # resolves the device's array outside the capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        run(side.cuda_stream)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for l in dst.store:
+            dst.store[l].copy_(fresh.store[l])
+        st.fill_(9)
+        other.unpack(0, noalloc=True)               # another plan's expansion into the same array
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0, f"replay {rep}: status {int(st.item())}"
+        host = dst.host(case.w.elem_bytes)
+        for l, want in case.expected[q].items():
+            assert np.array_equal(host[l], want), f"replay {rep}: layer {l} differs from the oracle"
+        print(f"[noalloc] graph replay {rep} matches the oracle", flush=True)

@@ -91,6 +91,11 @@ constexpr int kMaxUnitsPerWg = 128;   // (block, K or V) units per workgroup
 constexpr int64_t kSmallUnitBytes = 16 * 1024;   // units up to this size use the small policy
 constexpr int kSmallThreads = 128, kSmallUnroll = 4;
 constexpr int kPackSmallThreads = 64, kPackSmallUnroll = 4;   // pack of small units: one wave per unit
+// Pack of small units that take part of each row (the old rank's heads split among several new ranks,
+// e.g. 512 of 2048 bytes at TP1 -> TP4): four waves per unit with one vector per lane (A/B on MI355X,
+// one process, DeepSeek-32B share TP1/PP8 -> TP4/PP2: pack +3.7%; whole-row units stay faster with
+// one wave: 70B GQA -2.9%, Qwen3-30B-A3B -1.1% with this shape).
+constexpr int kPackPartialThreads = 256, kPackPartialUnroll = 1;
 // XCD-contiguous cell order, per launch kind (A/B on MI355X, one process: with it, 7B MHA pack
 // +5%; 70B GQA small-unit pack -1.5% and unpack of block-sorted descriptors -1.6%)
 constexpr bool kPackSmallXcd = false;

@@ -141,11 +141,15 @@ static remp_status launch_sort_new(int64_t n_desc, int64_t num_blocks, char* ws,
     return hip_check(hipGetLastError(), "descriptor sort launch");
 }
 
-// Launch shapes measured on MI355X (70B GQA and 7B MHA shares): small-unit pack runs one wave per
-// 4 KiB unit in plain grid order; everything else takes the XCD-contiguous cell order.
+// Launch shapes measured on MI355X (70B GQA, 7B MHA and DeepSeek-32B shares): small-unit pack runs
+// one wave per 4 KiB unit in plain grid order, or four waves of one vector per lane when its units
+// are parts of wider rows; everything else takes the XCD-contiguous cell order.
 template <int VEC, bool PACK, bool CHECK>
-static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_t stream) {
-    if (small && PACK)
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool partial, hipStream_t stream) {
+    if (small && PACK && partial)
+        hipLaunchKernelGGL((copy_slices<VEC, true, kPackPartialThreads, kPackPartialUnroll, kPackSmallXcd, CHECK>),
+                           grid, dim3(kPackPartialThreads), 0, stream, a);
+    else if (small && PACK)
         hipLaunchKernelGGL((copy_slices<VEC, true, kPackSmallThreads, kPackSmallUnroll, kPackSmallXcd, CHECK>), grid,
                            dim3(kPackSmallThreads), 0, stream, a);
     else if (small)
@@ -158,11 +162,11 @@ static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_
 }
 
 template <int VEC, bool PACK>
-static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, hipStream_t stream) {
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool partial, hipStream_t stream) {
     if (a.check.at[0] || a.check.at[1])
-        launch_copy_vec<VEC, PACK, true>(a, grid, small, stream);
+        launch_copy_vec<VEC, PACK, true>(a, grid, small, partial, stream);
     else
-        launch_copy_vec<VEC, PACK, false>(a, grid, small, stream);
+        launch_copy_vec<VEC, PACK, false>(a, grid, small, partial, stream);
 }
 
 template <bool PACK>
@@ -174,10 +178,12 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     // widest vector every address and stride is aligned to
     uint64_t bits = static_cast<uint64_t>(block_stride) | static_cast<uint64_t>(row_stride) | 16u;
     uint32_t max_row = 0;
+    bool partial = false;   // some slice takes only part of each row
     for (const HostSlice& s : slices) {
         bits |= s.paged_k | s.paged_v | s.stage | s.row_bytes |
                 (static_cast<uint64_t>(p.total_tokens) * s.row_bytes);
         max_row = std::max(max_row, s.row_bytes);
+        partial |= static_cast<int64_t>(s.row_bytes) < row_stride;
     }
     const int vec = static_cast<int>(bits & (~bits + 1));   // lowest set bit, <= 16
     const int64_t per_unit = static_cast<int64_t>(bs) * max_row;
@@ -201,7 +207,8 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     a.block_size = bs;
     a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
-    const int threads = small ? (PACK ? kPackSmallThreads : kSmallThreads) : kLargeThreads;
+    const int threads = small ? (PACK ? (partial ? kPackPartialThreads : kPackSmallThreads) : kSmallThreads)
+                              : kLargeThreads;
     if (remp_status st = check_grid(gx, kMaxItems, threads, PACK ? "pack" : "unpack")) return st;
 
     if (g_trace_start) {
@@ -225,11 +232,11 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
         }
         const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
         switch (vec) {
-            case 16: launch_copy_vec<16, PACK>(a, grid, small, stream); break;
-            case 8: launch_copy_vec<8, PACK>(a, grid, small, stream); break;
-            case 4: launch_copy_vec<4, PACK>(a, grid, small, stream); break;
-            case 2: launch_copy_vec<2, PACK>(a, grid, small, stream); break;
-            default: launch_copy_vec<1, PACK>(a, grid, small, stream); break;
+            case 16: launch_copy_vec<16, PACK>(a, grid, small, partial, stream); break;
+            case 8: launch_copy_vec<8, PACK>(a, grid, small, partial, stream); break;
+            case 4: launch_copy_vec<4, PACK>(a, grid, small, partial, stream); break;
+            case 2: launch_copy_vec<2, PACK>(a, grid, small, partial, stream); break;
+            default: launch_copy_vec<1, PACK>(a, grid, small, partial, stream); break;
         }
         if (remp_status st = hip_check(hipGetLastError(), PACK ? "pack launch" : "unpack launch")) return st;
     }

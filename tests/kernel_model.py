@@ -54,6 +54,7 @@ EMIT_CHUNK = 1 << 23          # expand_emit lanes modelled at once
 
 # (threads, loads per lane, XCD cell order) of each launch kind
 PACK_SMALL = (64, 4, False)
+PACK_PARTIAL = (256, 1, False)      # small-unit pack whose slices take part of each row
 UNPACK_SMALL = (128, 4, False)
 LARGE = (1024, 2, True)
 ROWS_SMALL = (256, 2, False)
@@ -399,9 +400,11 @@ def copy_launches(slices: Sequence[Slice], n_desc: int, bs: int, block_stride: i
         return []
     bits = block_stride | row_stride | 16
     max_row = 0
+    partial = False
     for s in slices:
         bits |= s.paged_k | s.paged_v | s.stage | s.row_bytes | (total_tokens * s.row_bytes)
         max_row = max(max_row, s.row_bytes)
+        partial |= s.row_bytes < row_stride
     vec = lowest_bit(bits)
     per_unit = bs * max_row
     small = per_unit <= SMALL_UNIT_BYTES
@@ -412,7 +415,7 @@ def copy_launches(slices: Sequence[Slice], n_desc: int, bs: int, block_stride: i
     if bs * (max_row // vec) >= MAX_WG_VECTORS:
         raise ModelError("unsupported: a block exceeds the workgroup index space")
     gx = (2 * n_desc + C - 1) // C
-    shape = (PACK_SMALL if pack else UNPACK_SMALL) if small else LARGE
+    shape = ((PACK_PARTIAL if partial else PACK_SMALL) if pack else UNPACK_SMALL) if small else LARGE
     check_grid(gx, MAX_ITEMS, shape[0], "copy")
     out = []
     for f in range(0, len(slices), MAX_ITEMS):

@@ -90,6 +90,11 @@ constexpr int kMaxUnitsPerWg = 128;   // (block, K or V) units per workgroup
 // workgroups that move about 64 KiB.
 constexpr int64_t kSmallUnitBytes = 16 * 1024;   // units up to this size use the small policy
 constexpr int kSmallThreads = 128, kSmallUnroll = 4;
+// Unpack workgroups that move at most 4 KiB (one 4 KiB unit, as with one 256-byte head row per token
+// at 16 tokens per block) run one wave of 4 vectors per lane, so no lane idles (A/B on MI355X, one
+// process, Qwen3-30B-A3B share: unpack +2.5%; with 8 KiB units the 128-thread shape stays faster).
+constexpr int kUnpackTinyThreads = 64;
+constexpr int64_t kUnpackTinyWgBytes = 4 * 1024;
 constexpr int kPackSmallThreads = 64, kPackSmallUnroll = 4;   // pack of small units: one wave per unit
 // Pack of small units that take part of each row (the old rank's heads split among several new ranks,
 // e.g. 512 of 2048 bytes at TP1 -> TP4): four waves per unit with one vector per lane (A/B on MI355X,

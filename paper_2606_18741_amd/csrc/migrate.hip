@@ -145,13 +145,16 @@ static remp_status launch_sort_new(int64_t n_desc, int64_t num_blocks, char* ws,
 // one wave per 4 KiB unit in plain grid order, or four waves of one vector per lane when its units
 // are parts of wider rows; everything else takes the XCD-contiguous cell order.
 template <int VEC, bool PACK, bool CHECK>
-static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool partial, hipStream_t stream) {
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool partial, bool tiny, hipStream_t stream) {
     if (small && PACK && partial)
         hipLaunchKernelGGL((copy_slices<VEC, true, kPackPartialThreads, kPackPartialUnroll, kPackSmallXcd, CHECK>),
                            grid, dim3(kPackPartialThreads), 0, stream, a);
     else if (small && PACK)
         hipLaunchKernelGGL((copy_slices<VEC, true, kPackSmallThreads, kPackSmallUnroll, kPackSmallXcd, CHECK>), grid,
                            dim3(kPackSmallThreads), 0, stream, a);
+    else if (small && tiny)
+        hipLaunchKernelGGL((copy_slices<VEC, false, kUnpackTinyThreads, kSmallUnroll, kUnpackSmallXcd, CHECK>), grid,
+                           dim3(kUnpackTinyThreads), 0, stream, a);
     else if (small)
         hipLaunchKernelGGL((copy_slices<VEC, false, kSmallThreads, kSmallUnroll, kUnpackSmallXcd, CHECK>), grid,
                            dim3(kSmallThreads), 0, stream, a);
@@ -162,11 +165,11 @@ static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool parti
 }
 
 template <int VEC, bool PACK>
-static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool partial, hipStream_t stream) {
+static void launch_copy_vec(const CopyArgs& a, dim3 grid, bool small, bool partial, bool tiny, hipStream_t stream) {
     if (a.check.at[0] || a.check.at[1])
-        launch_copy_vec<VEC, PACK, true>(a, grid, small, partial, stream);
+        launch_copy_vec<VEC, PACK, true>(a, grid, small, partial, tiny, stream);
     else
-        launch_copy_vec<VEC, PACK, false>(a, grid, small, partial, stream);
+        launch_copy_vec<VEC, PACK, false>(a, grid, small, partial, tiny, stream);
 }
 
 template <bool PACK>
@@ -207,7 +210,9 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
     a.block_size = bs;
     a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
-    const int threads = small ? (PACK ? (partial ? kPackPartialThreads : kPackSmallThreads) : kSmallThreads)
+    const bool tiny = !PACK && static_cast<int64_t>(C) * per_unit <= kUnpackTinyWgBytes;
+    const int threads = small ? (PACK ? (partial ? kPackPartialThreads : kPackSmallThreads)
+                                      : (tiny ? kUnpackTinyThreads : kSmallThreads))
                               : kLargeThreads;
     if (remp_status st = check_grid(gx, kMaxItems, threads, PACK ? "pack" : "unpack")) return st;
 
@@ -232,11 +237,11 @@ static remp_status launch_copy(const remp_kv_plan_t& p, const std::vector<HostSl
         }
         const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt));
         switch (vec) {
-            case 16: launch_copy_vec<16, PACK>(a, grid, small, partial, stream); break;
-            case 8: launch_copy_vec<8, PACK>(a, grid, small, partial, stream); break;
-            case 4: launch_copy_vec<4, PACK>(a, grid, small, partial, stream); break;
-            case 2: launch_copy_vec<2, PACK>(a, grid, small, partial, stream); break;
-            default: launch_copy_vec<1, PACK>(a, grid, small, partial, stream); break;
+            case 16: launch_copy_vec<16, PACK>(a, grid, small, partial, tiny, stream); break;
+            case 8: launch_copy_vec<8, PACK>(a, grid, small, partial, tiny, stream); break;
+            case 4: launch_copy_vec<4, PACK>(a, grid, small, partial, tiny, stream); break;
+            case 2: launch_copy_vec<2, PACK>(a, grid, small, partial, tiny, stream); break;
+            default: launch_copy_vec<1, PACK>(a, grid, small, partial, tiny, stream); break;
         }
         if (remp_status st = hip_check(hipGetLastError(), PACK ? "pack launch" : "unpack launch")) return st;
     }

@@ -55,6 +55,8 @@ EMIT_CHUNK = 1 << 23          # expand_emit lanes modelled at once
 # (threads, loads per lane, XCD cell order) of each launch kind
 PACK_SMALL = (64, 4, False)
 PACK_PARTIAL = (256, 1, False)      # small-unit pack whose slices take part of each row
+UNPACK_TINY = (64, 4, False)        # small-unit unpack moving at most 4 KiB per workgroup
+UNPACK_TINY_WG_BYTES = 4 * 1024
 UNPACK_SMALL = (128, 4, False)
 LARGE = (1024, 2, True)
 ROWS_SMALL = (256, 2, False)
@@ -415,7 +417,9 @@ def copy_launches(slices: Sequence[Slice], n_desc: int, bs: int, block_stride: i
     if bs * (max_row // vec) >= MAX_WG_VECTORS:
         raise ModelError("unsupported: a block exceeds the workgroup index space")
     gx = (2 * n_desc + C - 1) // C
-    shape = ((PACK_PARTIAL if partial else PACK_SMALL) if pack else UNPACK_SMALL) if small else LARGE
+    tiny = not pack and C * per_unit <= UNPACK_TINY_WG_BYTES
+    shape = ((PACK_PARTIAL if partial else PACK_SMALL) if pack else (UNPACK_TINY if tiny else UNPACK_SMALL)) \
+        if small else LARGE
     check_grid(gx, MAX_ITEMS, shape[0], "copy")
     out = []
     for f in range(0, len(slices), MAX_ITEMS):

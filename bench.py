@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--summarize-trace", default=None, metavar="STATS_CSV",
                     help="print a markdown table of a rocprofv3 --stats kernel summary (the library's kernels), "
                          "then exit")
+    ap.add_argument("--counter-filter", default=None, metavar="REGEX",
+                    help="with --summarize-counters: the --kernel-include-regex the two counter passes ran with "
+                         "(recorded in the commands of the record)")
     ap.add_argument("--calibration-gib", type=float, default=4.0,
                     help="size of the --library-calibration pool that the summarized calibration CSVs came from")
     ap.add_argument("--ceiling", type=float, default=0.0, metavar="GIB",
@@ -264,13 +267,14 @@ def summarize_counters(args) -> int:
     cal_bytes = _calibration_bytes(args.calibration_gib)
     fetch_scale = cal_bytes / (cal_fetch * 1024)
     write_scale = cal_bytes / (cal_write * 1024)
+    flt = f' --kernel-include-regex "{args.counter_filter}"' if args.counter_filter else ""
     out = {"workload": w.name + ": " + w.description, "source_hash": source_hash(),
            "note": "counters of the last 3 pack and 3 unpack calls of a --counter-pass run, summed over the copy "
                    "launches of a call (a call launches once per 8 slices, or per 8 layers for whole rows), "
                    "median over calls, KiB scaled by the library-calibration factors",
-           "commands": [f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc/{w.name}_fetch -o f -- "
+           "commands": [f"rocprofv3 --pmc FETCH_SIZE{flt} --output-format csv -d gpurun_out/pmc/{w.name}_fetch -o f -- "
                         f"python bench.py --workload {w.name} --counter-pass",
-                        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc/{w.name}_write -o w -- "
+                        f"rocprofv3 --pmc WRITE_SIZE{flt} --output-format csv -d gpurun_out/pmc/{w.name}_write -o w -- "
                         f"python bench.py --workload {w.name} --counter-pass",
                         f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc/cal_fetch -o f -- "
                         f"python bench.py --library-calibration {args.calibration_gib}",

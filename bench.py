@@ -319,8 +319,9 @@ def summarize_trace(path: str) -> int:
 
 
 def ceiling(args) -> int:
-    """HBM access-pattern probes: 4 and 8 KiB chunks copied, read or written in address order or through a
-    random permutation (optionally random only within windows of --ceiling-window MiB), each at every launch
+    """HBM access-pattern probes: 4 and 8 KiB chunks copied (with non-temporal or with device-scope stores),
+    read or written in address order or through a random permutation (optionally random only within windows
+    of --ceiling-window MiB), each at every launch
     shape (or --ceiling-shape), median of 3 launches; GB/s counts bytes read plus bytes written.  The copy
     patterns are rerun at their best shape into a cleared destination and checked chunk by chunk."""
     gib = args.ceiling
@@ -339,7 +340,9 @@ def ceiling(args) -> int:
     patterns = [("copy, contiguous", 0, False, False), ("copy, random reads (gather)", 0, True, False),
                 ("copy, random writes (scatter)", 0, False, True), ("copy, random reads and writes", 0, True, True),
                 ("read only, contiguous", 1, False, False), ("read only, random", 1, True, False),
-                ("write only, contiguous", 2, False, False), ("write only, random", 2, False, True)]
+                ("write only, contiguous", 2, False, False), ("write only, random", 2, False, True),
+                ("copy with device-scope stores, contiguous", 3, False, False),
+                ("copy with device-scope stores, random reads", 3, True, False)]
     results = []
     for chunk in [int(x) for x in args.ceiling_chunks.split(",")]:
         n = int(gib * (1 << 30)) // chunk
@@ -356,7 +359,7 @@ def ceiling(args) -> int:
         perm_r, perm_w = order(), order()
         sink = torch.empty(1024 * 16, dtype=torch.uint8, device="cuda")
         for name, mode, rr, rw in patterns:
-            moved = (2 if mode == 0 else 1) * n * chunk
+            moved = (2 if mode in (0, 3) else 1) * n * chunk
             best = None
             for (t, u, c) in shapes:
                 call = (mode, src.data_ptr(), dst.data_ptr(), sink.data_ptr(), sink.numel(), n, chunk,
@@ -377,7 +380,7 @@ def ceiling(args) -> int:
                 gbps = moved / statistics.median(ts) / 1e6
                 if best is None or gbps > best[0]:
                     best = (gbps, t, u, c)
-            if mode == 0:
+            if mode in (0, 3):
                 # the best shape once more into a cleared destination: chunk dst_idx[i] must hold chunk src_idx[i]
                 dst.zero_()
                 fn(mode, src.data_ptr(), dst.data_ptr(), sink.data_ptr(), sink.numel(), n, chunk,

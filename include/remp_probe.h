@@ -27,7 +27,9 @@ extern "C" {
  * destination chunk, mode 1 only reads the source chunks (each lane folds
  * what it read into a value that a store to `sink`, threads * 16 bytes of
  * device memory, would write on a condition that practically never holds),
- * mode 2 only writes the destination chunks.  All accesses are 16-byte non-temporal loads and stores.
+ * mode 2 only writes the destination chunks, mode 3 copies like mode 0 but
+ * stores at device scope (written through the L2 instead of held there).
+ * Other accesses are 16-byte non-temporal loads and stores.
  * chunk_bytes: a power of two >= 16.  threads: 256, 512 or 1024; unroll
  * (16-byte vectors in flight per lane): 1, 2, 4 or 8; chunks_per_wg >= 1;
  * ceil(n_chunks / chunks_per_wg) * threads below 2^32.

@@ -13,11 +13,18 @@ namespace {
 
 typedef unsigned int V4 __attribute__((ext_vector_type(4)));
 
+// 16-byte store at device scope: written through the XCD's L2 rather than held
+// there as a dirty line.
+__device__ __forceinline__ void store_device_scope(V4 v, V4* p) {
+    asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
+
 // One workgroup takes `cpw` consecutive entries of the chunk list; its lanes
 // stride over the (chunk, 16-byte vector) space with UNROLL vectors in flight.
 // Entry i moves chunk src_idx[i] of src to chunk dst_idx[i] of dst (identity
 // when an index array is NULL).  MODE 0 copies, 1 only reads (each lane folds what
-// it read into a register that a practically never taken store keeps alive), 2 only writes.
+// it read into a register that a practically never taken store keeps alive), 2 only writes,
+// 3 copies with device-scope stores.
 template <int THREADS, int UNROLL, int MODE>
 __global__ __launch_bounds__(THREADS) void chunk_probe(const char* __restrict__ src, char* __restrict__ dst,
                                                        V4* __restrict__ sink, int64_t n_chunks, uint32_t chunk_vecs,
@@ -55,6 +62,7 @@ __global__ __launch_bounds__(THREADS) void chunk_probe(const char* __restrict__ 
         for (int j = 0; j < UNROLL; ++j) {
             if (!ok[j]) continue;
             if (MODE == 1) acc ^= r[j];
+            else if (MODE == 3) store_device_scope(r[j], reinterpret_cast<V4*>(dst + d[j]));
             else __builtin_nontemporal_store(r[j], reinterpret_cast<V4*>(dst + d[j]));
         }
     }
@@ -67,7 +75,8 @@ hipError_t launch_mode(int32_t mode, dim3 grid, const char* src, char* dst, V4* 
                        uint32_t sh, const int32_t* si, const int32_t* di, int32_t cpw, hipStream_t s) {
     if (mode == 0) hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 0>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
     else if (mode == 1) hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 1>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
-    else hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 2>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
+    else if (mode == 2) hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 2>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
+    else hipLaunchKernelGGL((chunk_probe<THREADS, UNROLL, 3>), grid, dim3(THREADS), 0, s, src, dst, sink, n, cv, sh, si, di, cpw);
     return hipGetLastError();
 }
 
@@ -189,7 +198,7 @@ extern "C" {
 int32_t remp_probe_chunks(int32_t mode, const void* src, void* dst, void* sink, int64_t sink_bytes,
                           int64_t n_chunks, int32_t chunk_bytes, const int32_t* src_idx, const int32_t* dst_idx,
                           int32_t threads, int32_t unroll, int32_t chunks_per_wg, hipStream_t stream) {
-    if (mode < 0 || mode > 2) return -1;
+    if (mode < 0 || mode > 3) return -1;
     if (n_chunks <= 0 || chunk_bytes < 16 || (chunk_bytes & (chunk_bytes - 1)) != 0) return -1;
     if (threads != 256 && threads != 512 && threads != 1024) return -1;
     if (unroll != 1 && unroll != 2 && unroll != 4 && unroll != 8) return -1;

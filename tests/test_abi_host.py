@@ -76,7 +76,7 @@ def test_probe_library_exports_and_refuses_bad_arguments():
                    ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                    ctypes.c_void_p]
     ok = (0, 1 << 40, 1 << 41, None, 0, 16, 4096, None, None, 256, 2, 1, None)
-    for i, bad in ((0, 3), (6, 4000), (9, 128), (10, 3), (11, 0), (5, 0)):
+    for i, bad in ((0, 4), (0, -1), (6, 4000), (9, 128), (10, 3), (11, 0), (5, 0)):
         a = list(ok)
         a[i] = bad
         assert fn(*a) == -1, (i, bad)

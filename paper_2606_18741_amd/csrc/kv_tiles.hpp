@@ -250,6 +250,20 @@ __global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) 
 }
 
 
+// Leading slots that have a source among the m (4, 8 or 16) consecutive one-byte flags at p (1: the
+// row has a source), p aligned to m bytes: a ROCm V vector's slots in one or two LDS reads instead of
+// one per slot.
+__device__ __forceinline__ int32_t leading_sources(const uint8_t* p, int32_t m) {
+    if (m == 4) {
+        const uint32_t z = ~*reinterpret_cast<const uint32_t*>(p) & 0x01010101u;
+        return z ? static_cast<int32_t>(__builtin_ctz(z) >> 3) : 4;
+    }
+    const uint64_t z0 = ~*reinterpret_cast<const uint64_t*>(p) & 0x0101010101010101ull;
+    if (z0 || m == 8) return z0 ? static_cast<int32_t>(__builtin_ctzll(z0) >> 3) : 8;
+    const uint64_t z1 = ~*reinterpret_cast<const uint64_t*>(p + 8) & 0x0101010101010101ull;
+    return z1 ? 8 + static_cast<int32_t>(__builtin_ctzll(z1) >> 3) : 16;
+}
+
 // ---------------------------------------------------------------------------
 // local copy between pools of any layouts, one head tile at a time through LDS
 // ---------------------------------------------------------------------------
@@ -263,6 +277,12 @@ __global__ __launch_bounds__(kTileThreads) void copy_tiles(const TileArgs args) 
 // elements of one head lie block_size elements apart, is read element-wise.
 
 constexpr int kMaxLocalTileItems = 8;
+
+// Dynamic LDS of copy_local_tiles: `tiles` head tiles of bn rows of lds_row bytes, then per row an
+// 8-byte source base, a 4-byte slot and a 1-byte flag.
+inline int64_t local_tile_lds_bytes(int64_t tiles, int64_t bn, int64_t lds_row) {
+    return tiles * bn * lds_row + tiles * bn * 13;
+}
 
 struct LocalTileItem {
     uint64_t src_k, src_v;   // old storage of the layer at the slice's first head (block 0)
@@ -300,8 +320,6 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
     __shared__ uint64_t s_dst[kMaxUnitsPerWg];
     __shared__ int32_t s_n[kMaxUnitsPerWg];
     __shared__ int32_t s_kv[kMaxUnitsPerWg];
-    __shared__ uint64_t s_src[kMaxLocalRows];    // old tile (block, head) base of each (unit, row), 0: none
-    __shared__ int32_t s_slot[kMaxLocalRows];
 
     if (stale_descriptors(a.check)) return;
     const LocalTileItem& it = a.items[blockIdx.y];
@@ -312,6 +330,13 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
     const int32_t nt = static_cast<int32_t>(min(static_cast<int64_t>(a.tiles_per_wg), ntiles - g0));
     const int tid = threadIdx.x;
     const int32_t bn = a.new_block_size, bo = a.old_block_size, hb = a.head_bytes, eb = a.elem_bytes;
+    // per-(unit, row) arrays behind the tiles in the dynamic LDS, sized by the launch for tiles_per_wg
+    // units (local_tile_lds_bytes), so that the workgroup holds only what its units need
+    const uint32_t rows_cap = static_cast<uint32_t>(a.tiles_per_wg) * bn;
+    unsigned char* rows_lds = lds + static_cast<uint32_t>(a.tiles_per_wg) * bn * static_cast<uint32_t>(a.lds_row);
+    uint64_t* s_src = reinterpret_cast<uint64_t*>(rows_lds);               // old tile base of each row, 0: none
+    int32_t* s_slot = reinterpret_cast<int32_t*>(rows_lds + rows_cap * 8);  // its old slot
+    uint8_t* s_has = reinterpret_cast<uint8_t*>(rows_lds + rows_cap * 12);  // 1: the row has a source
 
     for (int i = tid; i < nt; i += kTileThreads) {
         const int64_t g = g0 + i;
@@ -352,6 +377,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
         }
         s_src[x] = base;
         s_slot[x] = slot;
+        s_has[x] = base != 0;
     }
     __syncthreads();
 
@@ -388,9 +414,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
                 const uint32_t e0 = v * m;
                 const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
                 const uint32_t s0 = e0 - dim * bn;
-                int32_t live = min(m, n - static_cast<int32_t>(s0));
-                for (int k = 0; k < live; ++k)
-                    if (s_src[i * bn + s0 + k] == 0) live = k;
+                const int32_t live = min(min(m, n - static_cast<int32_t>(s0)), leading_sources(s_has + i * bn + s0, m));
                 if (live <= 0) continue;
                 const V4 val = __builtin_nontemporal_load(src);
                 if (live == m) __builtin_nontemporal_store(val, dst);
@@ -466,9 +490,8 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
             const uint32_t e0 = v * m;
             const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
             const uint32_t s0 = e0 - dim * bn;
-            int32_t live = min(m, n - static_cast<int32_t>(s0));
-            for (int k = 0; k < live; ++k)                              // rows without a source stay untouched
-                if (s_src[i * bn + s0 + k] == 0) live = k;
+            // rows without a source stay untouched
+            const int32_t live = min(min(m, n - static_cast<int32_t>(s0)), leading_sources(s_has + i * bn + s0, m));
             if (live <= 0) continue;
             const V4 val = gather_dim(tl + s0 * lrow + dim * eb, lrow, eb);
             if (live == m) __builtin_nontemporal_store(val, dst);

@@ -686,7 +686,7 @@ static remp_status launch_local_tiles(const remp_kv_plan_t& p, const std::vector
         if (remp_status st = check_grid(gx, kMaxLocalTileItems, kTileThreads, "local head tiles")) return st;
         // 32-bit vector indices per workgroup: T tiles of bn rows of hb / 16 vectors
         hipLaunchKernelGGL(copy_local_tiles, dim3(static_cast<uint32_t>(gx), static_cast<uint32_t>(cnt)),
-                           dim3(kTileThreads), static_cast<size_t>(T * tile_lds), stream, a);
+                           dim3(kTileThreads), static_cast<size_t>(local_tile_lds_bytes(T, bn, lds_row)), stream, a);
         if (remp_status st = hip_check(hipGetLastError(), "copy_local_tiles launch")) return st;
     }
     if (g_trace_stop) {

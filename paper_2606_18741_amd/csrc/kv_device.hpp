@@ -115,8 +115,12 @@ constexpr int64_t kSmallWgBytes = 4 * 1024;
 // The local copy's per-unit prologue (three dependent descriptor reads) wants several units per
 // workgroup: 16 KiB against 8 KiB, copy_local alone on MI355X (one process, memory prewarmed):
 // 70B GQA -4.7% time, long context -5.8%, Qwen3-30B-A3B -5.6% (DeepSeek-32B -3.6% without the
-// prewarm); 256 threads or 32 KiB were slower (8 KiB against 4 KiB had been +14%).
+// prewarm); 256 x 4 or 32 KiB were slower (8 KiB against 4 KiB had been +14%).
 constexpr int64_t kLocalSmallWgBytes = 16 * 1024;
+// and 256 threads with two loads in flight per lane (one process, five repetitions, against 128 x 4):
+// 70B GQA -2.3% time, long context -1.1%, Qwen3-30B-A3B -2.0%, DeepSeek-32B +0.4%; 512 x 1, and 256 x 2
+// with 8 or 32 KiB per workgroup, were 3-9% slower than 128 x 4.
+constexpr int kLocalSmallThreads = 256, kLocalSmallUnroll = 2;
 // Large units (MHA rows of 2 KiB and more): 16-wave workgroups with two loads in flight per lane,
 // against 4 waves with eight (MI355X, one process, three repetitions): 7B MHA step -3.4%, 13B MHA
 // pack -2.1% and unpack -2.9% time.  The local copy's optimum differs: 512 x 4 was faster than

@@ -604,7 +604,8 @@ struct HostLocal {
 template <int VEC>
 static remp_status launch_local_vec(const LocalArgs& a, dim3 grid, bool small, hipStream_t stream) {
     if (small)
-        hipLaunchKernelGGL((copy_local<VEC, kSmallThreads, kSmallUnroll, false>), grid, dim3(kSmallThreads), 0, stream, a);
+        hipLaunchKernelGGL((copy_local<VEC, kLocalSmallThreads, kLocalSmallUnroll, false>), grid, dim3(kLocalSmallThreads), 0,
+                           stream, a);
     else
         hipLaunchKernelGGL((copy_local<VEC, kLocalLargeThreads, kLocalLargeUnroll, kLocalLargeXcd>), grid, dim3(kLocalLargeThreads), 0,
                            stream, a);
@@ -740,7 +741,7 @@ static remp_status launch_local(const remp_kv_plan_t& p, const std::vector<HostL
     a.new_block_size = bn;
     a.check = check;
     const int64_t gx = (2 * n_desc + C - 1) / C;
-    if (remp_status st = check_grid(gx, kMaxLocalItems, small ? kSmallThreads : kLocalLargeThreads, "local copy"))
+    if (remp_status st = check_grid(gx, kMaxLocalItems, small ? kLocalSmallThreads : kLocalLargeThreads, "local copy"))
         return st;
     if (g_trace_start) {
         if (remp_status st = hip_check(hipEventRecord(g_trace_start, stream), "trace start event")) return st;

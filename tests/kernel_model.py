@@ -61,7 +61,7 @@ UNPACK_SMALL = (128, 4, False)
 LARGE = (1024, 2, True)
 ROWS_SMALL = (256, 2, False)
 ROWS_LARGE = (1024, 2, True)
-LOCAL_SMALL = (128, 4, False)
+LOCAL_SMALL = (256, 2, False)
 LOCAL_LARGE = (512, 4, True)
 
 

@@ -276,9 +276,9 @@ def summarize_counters(args) -> int:
                         f"python bench.py --workload {w.name} --counter-pass",
                         f"rocprofv3 --pmc WRITE_SIZE{flt} --output-format csv -d gpurun_out/pmc/{w.name}_write -o w -- "
                         f"python bench.py --workload {w.name} --counter-pass",
-                        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc/cal_fetch -o f -- "
+                        f"rocprofv3 --pmc FETCH_SIZE{flt} --output-format csv -d gpurun_out/pmc/cal_fetch -o f -- "
                         f"python bench.py --library-calibration {args.calibration_gib}",
-                        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc/cal_write -o w -- "
+                        f"rocprofv3 --pmc WRITE_SIZE{flt} --output-format csv -d gpurun_out/pmc/cal_write -o w -- "
                         f"python bench.py --library-calibration {args.calibration_gib}",
                         f"python bench.py --workload {w.name} --calibration-gib {args.calibration_gib} "
                         f"--summarize-counters <the four CSVs>"],

@@ -737,6 +737,19 @@ def _live_prefix(n: np.ndarray, s0: np.ndarray, m: int, has_src: Optional[np.nda
     return live
 
 
+def _check_flag_reads(T: int, bn: int, lrow: int, tile: np.ndarray, s0: np.ndarray, m: int, what: str):
+    """copy_local_tiles reads a ROCm V vector's m one-byte source flags as one 4-byte (m = 4) or one or two
+    8-byte LDS words at byte tile * bn + s0 of the flag array, which follows the tiles (T * bn * lrow
+    bytes), the 8-byte source bases and the 4-byte slots (T * bn rows each) in the dynamic LDS: the
+    read must be aligned to its word and stay within the tile's own rows."""
+    rows_cap = T * bn
+    base = rows_cap * lrow
+    word = 4 if m == 4 else 8
+    off = base + rows_cap * 12 + tile * bn + s0
+    if base % 8 or (off % word).any() or (s0 + m > bn).any() or (s0 < 0).any():
+        raise ModelError(f"{what}: a vector's source flags are not aligned words within its tile's rows")
+
+
 def _store_prefixes(mem: Mem, dst: np.ndarray, vals: np.ndarray, live: np.ndarray, eb: int, m: int, what: str):
     for k in range(1, m + 1):
         sel = live == k
@@ -943,6 +956,8 @@ def run_copy_local_tiles(mem: Mem, L: Launch, ws: dict, workgroups: Optional[np.
                   "copy_local_tiles: store")
         if ln == ROCM:
             dim, s0 = div_checked(v * m, bn)
+            vv = (kk == 1) & (src0 != 0)
+            _check_flag_reads(T, bn, lrow, ti[xt][vv], s0[vv], m, "copy_local_tiles")
             rowsk = np.minimum(s0[:, None] + np.arange(m), bn - 1)
             live = _live_prefix(nn, s0, m, has_src[xt[:, None], rowsk])
             vm = (kk == 1) & (src0 != 0) & (live > 0)
@@ -983,6 +998,7 @@ def run_copy_local_tiles(mem: Mem, L: Launch, ws: dict, workgroups: Optional[np.
     mem.store(dst[kmask], lds.load(w_[kmask], tl[kmask] + rK[kmask] * lrow + cK[kmask] * 16, 16),
               "copy_local_tiles: store")
     dim, s0 = div_checked(v * m, bn)
+    _check_flag_reads(T, bn, lrow, ti[xt][kk == 1], s0[kk == 1], m, "copy_local_tiles")
     rowsk = np.minimum(s0[:, None] + np.arange(m), bn - 1)
     live = _live_prefix(nn, s0, m, has_src[xt[:, None], rowsk])
     vm = (kk == 1) & (live > 0)

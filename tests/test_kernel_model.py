@@ -301,3 +301,18 @@ def test_model_catches_the_planted_negative_token_mistake(monkeypatch):
     with pytest.raises(km.ModelError):
         for r in range(min(m.old.tp * m.old.pp, m.new.tp * m.new.pp)):
             m.copy_local(r)
+
+
+def test_flag_reads_check():
+    """The check of the local tile copy's source-flag reads accepts the word groups every ROCm V vector
+    reads (block sizes that are multiples of the vector's elements) and rejects a group that is
+    misaligned or runs past its tile's rows."""
+    for bn, m, T in ((16, 8, 4), (32, 16, 2), (8, 4, 7), (64, 8, 1)):
+        lrow = 16 * 17
+        s0 = np.arange(0, bn, m)
+        tiles = np.repeat(np.arange(T), s0.size)
+        km._check_flag_reads(T, bn, lrow, tiles, np.tile(s0, T), m, "ok")
+    with pytest.raises(km.ModelError):
+        km._check_flag_reads(4, 16, 272, np.array([1]), np.array([4]), 8, "misaligned")
+    with pytest.raises(km.ModelError):
+        km._check_flag_reads(4, 12, 272, np.array([0]), np.array([8]), 8, "past the tile")

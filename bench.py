@@ -99,6 +99,9 @@ def parse():
                     help="chunk sizes of the probes in bytes, comma separated")
     ap.add_argument("--ceiling-window", type=float, default=0.0, metavar="MIB",
                     help="draw the random chunk orders within consecutive windows of this many MiB (0: whole buffer)")
+    ap.add_argument("--ceiling-offset", type=int, default=0, metavar="BYTES",
+                    help="start every chunk this many bytes (a multiple of 16 below the chunk size) past a chunk "
+                         "boundary of the allocation, as staging pieces that start at any token do")
     ap.add_argument("--phased", type=float, default=0.0, metavar="GIB",
                     help="only run the phased-copy probe (a persistent copy whose workgroups wait for each other "
                          "between loads and stores, so the chip reads and writes in separate phases) next to the "
@@ -321,7 +324,7 @@ def summarize_trace(path: str) -> int:
 def ceiling(args) -> int:
     """HBM access-pattern probes: 4 and 8 KiB chunks copied (with non-temporal or with device-scope stores),
     read or written in address order or through a random permutation (optionally random only within windows
-    of --ceiling-window MiB), each at every launch
+    of --ceiling-window MiB; every chunk --ceiling-offset bytes past a chunk boundary), each at every launch
     shape (or --ceiling-shape), median of 3 launches; GB/s counts bytes read plus bytes written.  The copy
     patterns are rerun at their best shape into a cleared destination and checked chunk by chunk."""
     gib = args.ceiling
@@ -346,9 +349,15 @@ def ceiling(args) -> int:
     results = []
     for chunk in [int(x) for x in args.ceiling_chunks.split(",")]:
         n = int(gib * (1 << 30)) // chunk
-        src = torch.randint(0, 256, (n * chunk,), dtype=torch.uint8, device="cuda",
-                            generator=torch.Generator(device="cuda").manual_seed(chunk))
-        dst = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
+        off = args.ceiling_offset
+        if off % 16 or not 0 <= off < chunk:
+            raise SystemExit(f"--ceiling-offset {off}: a multiple of 16 below the chunk size {chunk} is needed")
+        # the chunks start `off` bytes into the allocations (one chunk more is allocated when off > 0)
+        extra = chunk if off else 0
+        src_all = torch.randint(0, 256, (n * chunk + extra,), dtype=torch.uint8, device="cuda",
+                                generator=torch.Generator(device="cuda").manual_seed(chunk))
+        dst_all = torch.empty(n * chunk + extra, dtype=torch.uint8, device="cuda")
+        src, dst = src_all[off:off + n * chunk], dst_all[off:off + n * chunk]
         g = torch.Generator(device="cpu").manual_seed(chunk)
         win = max(1, int(args.ceiling_window * (1 << 20)) // chunk) if args.ceiling_window > 0 else n
 
@@ -397,10 +406,11 @@ def ceiling(args) -> int:
                             "frac_of_peak": round(best[0] / PEAK_HBM_GBS, 4),
                             "best_shape": {"threads": best[1], "unroll": best[2], "chunks_per_workgroup": best[3]}})
             log(f"ceiling {chunk} B {name}: {best[0]:.1f} GB/s ({best[1]} x {best[2]}, {best[3]} chunks per workgroup)")
-        del src, dst, perm_r, perm_w, sink
+        del src, dst, src_all, dst_all, perm_r, perm_w, sink
         torch.cuda.empty_cache()
     print(json.dumps({"metric": "HBM access-pattern ceiling", "unit": "GB/s (read + write)", "buffer_GiB": gib,
-                      "random_window_MiB": args.ceiling_window or None, "shapes_tried": len(shapes),
+                      "random_window_MiB": args.ceiling_window or None, "chunk_offset_bytes": args.ceiling_offset,
+                      "shapes_tried": len(shapes),
                       "results": results}))
     return 0
 

@@ -279,9 +279,9 @@ __device__ __forceinline__ int32_t leading_sources(const uint8_t* p, int32_t m) 
 constexpr int kMaxLocalTileItems = 8;
 
 // Dynamic LDS of copy_local_tiles: `tiles` head tiles of bn rows of lds_row bytes, then per row an
-// 8-byte source base, a 4-byte slot and a 1-byte flag.
+// 8-byte source base, a 4-byte slot and a 1-byte flag, then a 1-byte flag per tile.
 inline int64_t local_tile_lds_bytes(int64_t tiles, int64_t bn, int64_t lds_row) {
-    return tiles * bn * lds_row + tiles * bn * 13;
+    return tiles * bn * lds_row + tiles * bn * 13 + tiles;
 }
 
 struct LocalTileItem {
@@ -337,6 +337,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
     uint64_t* s_src = reinterpret_cast<uint64_t*>(rows_lds);               // old tile base of each row, 0: none
     int32_t* s_slot = reinterpret_cast<int32_t*>(rows_lds + rows_cap * 8);  // its old slot
     uint8_t* s_has = reinterpret_cast<uint8_t*>(rows_lds + rows_cap * 12);  // 1: the row has a source
+    uint8_t* s_full = s_has + rows_cap;       // per tile, 1: every row live and with a source
 
     for (int i = tid; i < nt; i += kTileThreads) {
         const int64_t g = g0 + i;
@@ -348,7 +349,9 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
                    static_cast<uint64_t>(j) * a.new_head_step;
         s_n[i] = nd.n;
         s_kv[i] = kv;
+        s_full[i] = nd.n == bn;
     }
+    __syncthreads();
     for (int x = tid; x < nt * bn; x += kTileThreads) {
         const int32_t i = x / bn, r = x - (x / bn) * bn;
         const int64_t g = g0 + i;
@@ -378,6 +381,7 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
         s_src[x] = base;
         s_slot[x] = slot;
         s_has[x] = base != 0;
+        if (base == 0) s_full[i] = 0;
     }
     __syncthreads();
 
@@ -400,7 +404,9 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
             if (src0 == 0) continue;
             const V4* src = reinterpret_cast<const V4*>(src0 + uint64_t(v) * 16);
             V4* dst = reinterpret_cast<V4*>(s_dst[i] + uint64_t(v) * 16);
-            if (a.new_layout == kLayoutHND || s_kv[i] == 0) {
+            if (s_full[i]) {                                            // every vector of the tile is live
+                __builtin_nontemporal_store(__builtin_nontemporal_load(src), dst);
+            } else if (a.new_layout == kLayoutHND || s_kv[i] == 0) {
                 uint32_t r;
                 if (a.new_layout == kLayoutHND) {
                     r = fast_div(v, a.vph_magic, a.vph_shift);
@@ -417,6 +423,52 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
                 const int32_t live = min(min(m, n - static_cast<int32_t>(s0)), leading_sources(s_has + i * bn + s0, m));
                 if (live <= 0) continue;
                 const V4 val = __builtin_nontemporal_load(src);
+                if (live == m) __builtin_nontemporal_store(val, dst);
+                else store_prefix_bytes(val, dst, live * eb, eb);
+            }
+        }
+        return;
+    }
+
+    if (a.old_layout == a.new_layout) {
+        // Same tile layout, block sizes that differ: token t of a sequence sits at row t mod bn of its new
+        // block and at slot t mod bo of its old one, and both sizes are multiples of m (16 bytes of
+        // elements), so a 16-byte vector of a new tile, part of one row (HND, ROCm K) or m rows of one dim
+        // starting at a multiple of m (ROCm V), has one 16-byte source vector in an old tile: each is
+        // copied directly, without LDS.  A V vector is read at its first row's source; one whose slot is
+        // not a multiple of m (only when the device tables disagree with the host's) is not copied.
+        for (uint32_t x = tid; x < total; x += kTileThreads) {
+            const uint32_t i = fast_div(x, a.rows_magic, a.rows_shift);
+            const uint32_t v = x - i * per_tile;
+            const int32_t n = s_n[i];
+            V4* dst = reinterpret_cast<V4*>(s_dst[i] + uint64_t(v) * 16);
+            if (a.new_layout == kLayoutHND || s_kv[i] == 0) {
+                uint32_t r;
+                uint64_t off;                                            // within the old tile, but the slot
+                uint32_t slot_bytes;
+                if (a.new_layout == kLayoutHND) {                        // [slot][dim]
+                    r = fast_div(v, a.vph_magic, a.vph_shift);
+                    off = uint64_t(v - r * vph) * 16;
+                    slot_bytes = static_cast<uint32_t>(hb);
+                } else {                                                 // [dim / x][slot][x]
+                    const uint32_t c = fast_div(v, a.bn_magic, a.bn_shift);
+                    r = v - c * bn;
+                    off = uint64_t(c) * bo * 16;
+                    slot_bytes = 16;
+                }
+                if (static_cast<int32_t>(r) >= n || !s_has[i * bn + r]) continue;
+                const uint64_t src = s_src[i * bn + r] + off + uint64_t(s_slot[i * bn + r]) * slot_bytes;
+                __builtin_nontemporal_store(__builtin_nontemporal_load(reinterpret_cast<const V4*>(src)), dst);
+            } else {                                                     // [dim][slot]
+                const uint32_t e0 = v * m;
+                const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
+                const uint32_t s0 = e0 - dim * bn;
+                const int32_t live = min(min(m, n - static_cast<int32_t>(s0)), leading_sources(s_has + i * bn + s0, m));
+                if (live <= 0) continue;
+                const uint32_t slot = static_cast<uint32_t>(s_slot[i * bn + s0]);
+                if (slot & static_cast<uint32_t>(m - 1)) continue;
+                const V4 val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(
+                    s_src[i * bn + s0] + uint64_t(dim) * bo * eb + uint64_t(slot) * eb));
                 if (live == m) __builtin_nontemporal_store(val, dst);
                 else store_prefix_bytes(val, dst, live * eb, eb);
             }
@@ -468,10 +520,11 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
         const uint32_t v = x - i * per_tile;                            // vector of the tile in its own order
         const unsigned char* tl = lds + i * tile_lds;
         const int32_t n = s_n[i];
+        const bool full = s_full[i];
         if (a.new_layout == kLayoutNHD) {
             const uint32_t r = fast_div(v, a.vph_magic, a.vph_shift);
             const uint32_t c = v - r * vph;
-            if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+            if (full || (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0))
                 __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + r * lrow + c * 16),
                                             reinterpret_cast<V4*>(s_dst[i] + uint64_t(r) * a.new_row_stride + c * 16));
             continue;
@@ -479,19 +532,20 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
         V4* dst = reinterpret_cast<V4*>(s_dst[i] + uint64_t(v) * 16);
         if (a.new_layout == kLayoutHND) {
             const uint32_t r = fast_div(v, a.vph_magic, a.vph_shift);
-            if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+            if (full || (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0))
                 __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + r * lrow + (v - r * vph) * 16), dst);
         } else if (s_kv[i] == 0) {                                       // [dim / x][slot][x]
             const uint32_t c = fast_div(v, a.bn_magic, a.bn_shift);
             const uint32_t r = v - c * bn;
-            if (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0)
+            if (full || (static_cast<int32_t>(r) < n && s_src[i * bn + r] != 0))
                 __builtin_nontemporal_store(*reinterpret_cast<const V4*>(tl + r * lrow + c * 16), dst);
         } else {                                                         // [dim][slot]
             const uint32_t e0 = v * m;
             const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
             const uint32_t s0 = e0 - dim * bn;
             // rows without a source stay untouched
-            const int32_t live = min(min(m, n - static_cast<int32_t>(s0)), leading_sources(s_has + i * bn + s0, m));
+            const int32_t live =
+                full ? m : min(min(m, n - static_cast<int32_t>(s0)), leading_sources(s_has + i * bn + s0, m));
             if (live <= 0) continue;
             const V4 val = gather_dim(tl + s0 * lrow + dim * eb, lrow, eb);
             if (live == m) __builtin_nontemporal_store(val, dst);

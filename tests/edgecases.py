@@ -71,18 +71,19 @@ LIMITS = custom(name="limits", num_layers=1, num_kv_heads=1, head_dim=4, elem_by
                 pool_law=("slack", 1.001), old_topo=(1, 1), new_topo=(1, 1), role=(0, 0), seed=31)
 
 
-# Pool layout pairs (old, new) of the shifted-lengths case: NHD, HND and ROCm tiles, same and mixed.
-SHIFTED_LAYOUTS = [(0, 0), (1, 1), (2, 2), (0, 1)]
+# Pool layout pairs (old, new) and new block sizes of the shifted-lengths case: NHD, HND and ROCm tiles,
+# same and mixed, with the old block size (16) kept or doubled.
+SHIFTED_LAYOUTS = [(0, 0, 16), (1, 1, 16), (2, 2, 16), (0, 1, 16), (1, 1, 32), (2, 2, 32), (2, 0, 32)]
 
 
-def shifted_old_lengths_case():
+def shifted_old_lengths_case(new_block_size: int = 16):
     """Identity topology (every slice is local) and old device tables that disagree with the host ones:
     17 tokens move from sequence 1 to sequence 0 (same total, shifted starts), and sequence 1's first old
     block is physical block 0.  The local copies combine the new expansion's token offsets with the old
     one's, so the first 16 rows of sequence 1 get a negative token index.  Returns (workload, inputs,
     (device lengths, device row offsets, device block ids))."""
     w = custom(num_layers=2, num_kv_heads=8, head_dim=64, old_topo=(2, 1), new_topo=(2, 1), num_seqs=3,
-               length_law=("fixed", 40), seed=5)
+               length_law=("fixed", 40), seed=5, new_block_size=new_block_size)
     inp = synthkv.make_inputs(w)
     t = inp.old_tables
     lens = t.seq_lens.copy()

@@ -964,6 +964,29 @@ def run_copy_local_tiles(mem: Mem, L: Launch, ws: dict, workgroups: Optional[np.
             vals = mem.load(src0[vm] + v[vm] * 16, 16, "copy_local_tiles: load")
             _store_prefixes(mem, s_dst[xt][vm] + v[vm] * 16, vals, live[vm], eb, m, "copy_local_tiles: store")
         return int(flag)
+    if lo == ln:                                         # same layout, block sizes differ: vector from vector
+        if ln == HND:
+            rows, c = div_checked(v, vph)
+            off, sb = c * 16, hb
+        else:
+            c, rows = div_checked(v, bn)
+            off, sb = c * bo * 16, 16
+        plain = (ln == HND) | (kk == 0)
+        okv = plain & (rows < nn) & has_src[xt, rows]
+        src = s_src[xt, rows] + off + s_slot[xt, rows] * sb
+        mem.store(s_dst[xt][okv] + v[okv] * 16, mem.load(src[okv], 16, "copy_local_tiles: load"),
+                  "copy_local_tiles: store")
+        if ln == ROCM:
+            dim, s0 = div_checked(v * m, bn)
+            vv = kk == 1
+            _check_flag_reads(T, bn, lrow, ti[xt][vv], s0[vv], m, "copy_local_tiles")
+            rowsk = np.minimum(s0[:, None] + np.arange(m), bn - 1)
+            live = _live_prefix(nn, s0, m, has_src[xt[:, None], rowsk])
+            slot0 = s_slot[xt, s0]
+            vm = vv & (live > 0) & (slot0 % m == 0)
+            vals = mem.load(s_src[xt, s0][vm] + dim[vm] * bo * eb + slot0[vm] * eb, 16, "copy_local_tiles: load")
+            _store_prefixes(mem, s_dst[xt][vm] + v[vm] * 16, vals, live[vm], eb, m, "copy_local_tiles: store")
+        return int(flag)
     lds = LdsBank(bx.size, a["lds_bytes"])
     w_, tl = tw[xt], ti[xt] * tile_lds
     rows, c = div_checked(v, vph)

@@ -252,13 +252,13 @@ def test_mismatched_device_tables_are_contained():
         assert torch.equal(staging[p], before[p])
 
 
-@pytest.mark.parametrize("lo,ln", SHIFTED_LAYOUTS)
-def test_local_copy_contains_shifted_device_lengths(lo, ln):
+@pytest.mark.parametrize("lo,ln,bn", SHIFTED_LAYOUTS)
+def test_local_copy_contains_shifted_device_lengths(lo, ln, bn):
     """Old device lengths that shift a sequence start (same total) give some rows of the local copies a
     negative token index; those rows must be skipped and flagged, never read from before an old block.
     (The CPU model of the kernels checks this case access by access: test_model_shifted_old_lengths.)"""
     rk = _rk()
-    w, inp, (lens, offs, ids) = shifted_old_lengths_case()
+    w, inp, (lens, offs, ids) = shifted_old_lengths_case(bn)
     L = w.num_layers
     plan = rk.Plan(w.old_topo, w.new_topo, shape_of(w), rk.HostTables.of(inp.old_tables))
     old_host = hostpools.source_pools(w, inp.old_tables)

@@ -250,11 +250,11 @@ def test_model_full_size_layouts(lo, ln):
 # device tables that disagree with the host tables
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("lo,ln", SHIFTED_LAYOUTS)
-def test_model_shifted_old_lengths_are_contained(lo, ln):
+@pytest.mark.parametrize("lo,ln,bn", SHIFTED_LAYOUTS)
+def test_model_shifted_old_lengths_are_contained(lo, ln, bn):
     """The local copies combine the new expansion's token offsets with the old one's; old device lengths
     that shift a sequence start (same total) must neither leave the pools nor go unreported."""
-    w, inp, dev_old = _shifted_case()
+    w, inp, dev_old = _shifted_case(bn)
     m = km.Migration(w, inp, lo, ln, data=True, dev_old=dev_old)
     flags = [m.copy_local(r) for r in range(min(m.old.tp * m.old.pp, m.new.tp * m.new.pp))]
     assert all(f == 1 for f in flags), f"shifted device lengths went unreported: {flags}"

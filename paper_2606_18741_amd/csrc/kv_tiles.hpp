@@ -480,6 +480,35 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
     for (uint32_t x = tid; x < total; x += kTileThreads) {
         const uint32_t i = fast_div(x, a.rows_magic, a.rows_shift);
         const uint32_t rem = x - i * per_tile;
+        if (a.old_layout == kLayoutRocmSplit && s_kv[i] == 1) {
+            // [dim][slot] V tiles: vector rem holds m rows s0.. of one dim, whose old slots run on from a
+            // multiple of m in one old block (as in the same-layout copy), so it is read as one 16-byte vector
+            // at its first row's source and stored to LDS element by element; live rows outside that run
+            // (only when the device tables disagree with the host's) are read element by element
+            const uint32_t e0 = rem * m;
+            const uint32_t dim = fast_div(e0, a.bn_magic, a.bn_shift);
+            const uint32_t s0 = e0 - dim * bn;
+            const int32_t nl = min(m, s_n[i] - static_cast<int32_t>(s0));    // live rows of the vector
+            if (nl <= 0) continue;
+            unsigned char* t0 = lds + i * tile_lds + s0 * lrow + dim * eb;
+            const uint32_t slot0 = static_cast<uint32_t>(s_slot[i * bn + s0]);
+            const int32_t run = (slot0 & static_cast<uint32_t>(m - 1)) ? 0 : leading_sources(s_has + i * bn + s0, m);
+            if (run > 0)
+                scatter_dim(__builtin_nontemporal_load(reinterpret_cast<const V4*>(
+                                s_src[i * bn + s0] + uint64_t(dim) * bo * eb + uint64_t(slot0) * eb)),
+                            t0, lrow, eb);
+            for (int32_t k = run; k < nl; ++k) {
+                const uint32_t row = s0 + static_cast<uint32_t>(k);
+                if (!s_has[i * bn + row]) continue;
+                const unsigned char* e = reinterpret_cast<const unsigned char*>(s_src[i * bn + row]) +
+                                         uint64_t(dim) * bo * eb + uint64_t(s_slot[i * bn + row]) * eb;
+                unsigned char* o = t0 + k * lrow;
+                if (eb == 2) *reinterpret_cast<unsigned short*>(o) = *reinterpret_cast<const unsigned short*>(e);
+                else if (eb == 4) *reinterpret_cast<unsigned int*>(o) = *reinterpret_cast<const unsigned int*>(e);
+                else *o = *e;
+            }
+            continue;
+        }
         const uint32_t r = fast_div(rem, a.vph_magic, a.vph_shift);
         const uint32_t c = rem - r * vph;
         const uint64_t base = s_src[i * bn + r];
@@ -490,25 +519,8 @@ __global__ __launch_bounds__(kTileThreads) void copy_local_tiles(const LocalTile
             val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(base + uint64_t(slot) * a.old_row_stride + c * 16));
         } else if (a.old_layout == kLayoutHND) {
             val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(base + uint64_t(slot) * hb + c * 16));
-        } else if (s_kv[i] == 0) {                                       // [dim / x][slot][x]
+        } else {                                                         // [dim / x][slot][x] (K)
             val = __builtin_nontemporal_load(reinterpret_cast<const V4*>(base + uint64_t(c) * bo * 16 + slot * 16));
-        } else {                                                         // [dim][slot]: element-wise
-            // the vector's m elements lie bo elements apart; they are assembled in registers
-            const unsigned char* src = reinterpret_cast<const unsigned char*>(base) + uint64_t(c) * m * bo * eb +
-                                       uint64_t(slot) * eb;
-            const uint64_t st = uint64_t(bo) * eb;
-            if (eb == 2) {
-                const auto h = [&](int k) { return static_cast<unsigned int>(*reinterpret_cast<const unsigned short*>(src + k * st)); };
-                val = V4{h(0) | (h(1) << 16), h(2) | (h(3) << 16), h(4) | (h(5) << 16), h(6) | (h(7) << 16)};
-            } else if (eb == 4) {
-                const auto w = [&](int k) { return *reinterpret_cast<const unsigned int*>(src + k * st); };
-                val = V4{w(0), w(1), w(2), w(3)};
-            } else {
-                unsigned int w[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-                for (int k = 0; k < 16; ++k) w[k >> 2] |= static_cast<unsigned int>(src[k * st]) << (8 * (k & 3));
-                val = V4{w[0], w[1], w[2], w[3]};
-            }
         }
         *reinterpret_cast<V4*>(lds + i * tile_lds + r * lrow + c * 16) = val;
     }

@@ -998,15 +998,33 @@ def run_copy_local_tiles(mem: Mem, L: Launch, ws: dict, workgroups: Optional[np.
     elif lo == HND:
         val = mem.load(base[okr] + sl[okr] * hb + c[okr] * 16, 16, "copy_local_tiles: load")
     else:
-        kmask = okr & (kk == 0)
-        vmask = okr & (kk == 1)
-        val = np.zeros((int(okr.sum()), 16), np.uint8)
-        pos = np.cumsum(okr) - 1
-        val[pos[kmask]] = mem.load(base[kmask] + c[kmask] * bo * 16 + sl[kmask] * 16, 16, "copy_local_tiles: load")
-        if vmask.any():
-            e0 = (base[vmask] + c[vmask] * m * bo * eb + sl[vmask] * eb)[:, None] + np.arange(m) * bo * eb
-            val[pos[vmask]] = mem.load(e0.reshape(-1), eb, "copy_local_tiles: load").reshape(-1, 16)
-    lds.store(w_[okr], tl[okr] + rows[okr] * lrow + c[okr] * 16, val)
+        # K tiles as the other layouts; V tiles ([dim][slot]) by vectors of m rows of one dim (below)
+        okk = okr & (kk == 0)
+        val = mem.load(base[okk] + c[okk] * bo * 16 + sl[okk] * 16, 16, "copy_local_tiles: load")
+    if lo != ROCM:
+        lds.store(w_[okr], tl[okr] + rows[okr] * lrow + c[okr] * 16, val)
+    else:
+        lds.store(w_[okk], tl[okk] + rows[okk] * lrow + c[okk] * 16, val)
+    if lo == ROCM:
+        vv = kk == 1
+        dim, s0 = div_checked(v * m, bn)
+        nl = np.minimum(m, nn - s0)
+        _check_flag_reads(T, bn, lrow, ti[xt][vv & (nl > 0)], s0[vv & (nl > 0)], m, "copy_local_tiles")
+        rowsk = np.minimum(s0[:, None] + np.arange(m), bn - 1)
+        run = _live_prefix(nn, s0, m, has_src[xt[:, None], rowsk])
+        slot0 = s_slot[xt, s0]
+        run = np.where(slot0 % m == 0, run, 0)
+        vm = vv & (nl > 0) & (run > 0)
+        vals = mem.load(s_src[xt, s0][vm] + dim[vm] * bo * eb + slot0[vm] * eb, 16, "copy_local_tiles: load")
+        offs = (tl[vm] + dim[vm] * eb)[:, None] + (s0[vm][:, None] + np.arange(m)) * lrow
+        lds.store(np.repeat(w_[vm], m), offs.reshape(-1), vals.reshape(-1, eb))
+        for k in range(m):                               # live rows outside the run, element by element
+            r_ = np.minimum(s0 + k, bn - 1)
+            em = vv & (k >= np.maximum(run, 0)) & (k < nl) & has_src[xt, r_]
+            if em.any():
+                e = mem.load(s_src[xt, r_][em] + dim[em] * bo * eb + s_slot[xt, r_][em] * eb, eb,
+                             "copy_local_tiles: load")
+                lds.store(w_[em], tl[em] + (s0[em] + k) * lrow + dim[em] * eb, e)
     if ln == NHD:
         mem.store(s_dst[xt][okr] + rows[okr] * a["nrow"] + c[okr] * 16,
                   lds.load(w_[okr], tl[okr] + rows[okr] * lrow + c[okr] * 16, 16), "copy_local_tiles: store")

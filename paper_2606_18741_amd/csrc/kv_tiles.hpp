@@ -265,16 +265,18 @@ __device__ __forceinline__ int32_t leading_sources(const uint8_t* p, int32_t m) 
 }
 
 // ---------------------------------------------------------------------------
-// local copy between pools of any layouts, one head tile at a time through LDS
+// local copy between pools of any layouts (not both NHD), one head tile at a time
 // ---------------------------------------------------------------------------
 //
 // A unit is one (new block, K or V, head of the slice) tile.  The prologue
 // resolves each of its rows to the old (block, slot) through the old
-// descriptors; phase 1 reads every live row's head vectors from the old pool
-// in its layout into LDS (token-major); phase 2 writes the tile into the new
-// pool in its layout, live slots only.  NHD rows on either side are read or
-// written as 16-byte vectors of the row; the ROCm V layout, where a token's
-// elements of one head lie block_size elements apart, is read element-wise.
+// descriptors.  When both pools have the same layout, every 16-byte vector of
+// a new tile has one 16-byte source vector in an old tile and is copied
+// directly.  Otherwise the tile goes through LDS: phase 1 reads every live
+// row's head vectors from the old pool in its layout into LDS (token-major;
+// ROCm V tiles, where a token's elements of one head lie block_size elements
+// apart, as vectors of m rows of one dim, stored element by element); phase 2
+// writes the tile into the new pool in its layout, live slots only.
 
 constexpr int kMaxLocalTileItems = 8;
 

@@ -137,7 +137,9 @@ enum {
  * num_blocks blocks in `layout`.  Pointer arrays are host memory; entries for
  * layers outside the call's layer window may be NULL.  HND and ROCM_SPLIT need
  * head_dim * elem_bytes % 16 == 0 and 16-byte aligned storage; ROCM_SPLIT also
- * block_size * elem_bytes % 16 == 0 (REMP_E_UNSUPPORTED / REMP_E_ALIGN). */
+ * block_size * elem_bytes % 16 == 0 (REMP_E_UNSUPPORTED / REMP_E_ALIGN).  One
+ * (block, head) tile of such a pool must fit the copy kernels' LDS budget:
+ * block_size * (head_dim * elem_bytes + 16) <= 32768 (REMP_E_UNSUPPORTED). */
 typedef struct {
     int32_t num_layers;
     int32_t layout;
@@ -323,9 +325,10 @@ REMP_API remp_status remp_kv_unpack_noalloc(const remp_kv_plan_t* plan, int32_t 
  * unpack called with REMP_KV_SKIP_LOCAL this yields the same new pool as a
  * staged migration while moving the local share once instead of twice.
  * rank must exist in both topologies.  The two pools may have any layouts
- * (for HND or ROCM_SPLIT pools head tiles go through LDS; those layouts need
- * head_dim * elem_bytes % 16 == 0 and the new block size at most 1024,
- * REMP_E_UNSUPPORTED otherwise).  src and dst storage must not overlap
+ * (HND or ROCM_SPLIT pools are copied in head tiles, through LDS when the two
+ * layouts differ; those layouts need head_dim * elem_bytes % 16 == 0, a new
+ * block size of at most 1024 and new_block_size * (head_dim * elem_bytes + 16)
+ * <= 32768, REMP_E_UNSUPPORTED otherwise).  src and dst storage must not overlap
  * (checked per layer, REMP_E_INVALID).  new_tables are validated as in
  * remp_kv_unpack.  old_tables / new_dev_tables: device copies of the tables.
  * The workspace is the one remp_kv_workspace_bytes sizes; nothing is enqueued

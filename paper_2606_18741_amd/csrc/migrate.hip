@@ -459,6 +459,16 @@ static remp_status check_pool(const remp_kv_plan_t* plan, const remp_kv_pool* po
     return REMP_OK;
 }
 
+// A (block, head) tile of block_size rows of head_dim * elem_bytes bytes, each padded by 16 bytes, must fit
+// the head-tile kernels' LDS budget; checked with the other arguments, before anything is enqueued.
+static remp_status check_tile_fits(const remp_kv_plan_t* plan, int32_t block_size, const char* what) {
+    const int64_t hb = static_cast<int64_t>(plan->shape.head_dim) * plan->shape.elem_bytes;
+    if (static_cast<int64_t>(block_size) * (hb + 16) > kTileLdsBytes)
+        return fail(REMP_E_UNSUPPORTED, std::string(what) + ": a (block, head) tile of " + std::to_string(block_size) +
+                                            " rows does not fit the LDS budget of the head-tile kernels");
+    return REMP_OK;
+}
+
 static remp_status check_workspace(const remp_kv_plan_t* plan, void* ws, int64_t ws_bytes) {
     if (!ws) return fail(REMP_E_INVALID, "workspace is NULL");
     if (!aligned(ws, 256)) return fail(REMP_E_ALIGN, "workspace is not 256-byte aligned");
@@ -813,6 +823,8 @@ static remp_status unpack_impl(const remp_kv_plan_t* plan, int32_t new_rank, int
     if (remp_status st = collect_slices(*plan, false, new_rank, layer_begin, layer_end, *dst, staging,
                                         (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
         return st;
+    if (dst->layout != kLayoutNHD)
+        if (remp_status st = check_tile_fits(plan, plan->shape.new_block_size, "unpack")) return st;
     if (layer_begin == layer_end || plan->new_live_blocks == 0) return REMP_OK;   // as in pack
     const remp_kv_shape& sh = plan->shape;
     const int64_t row_stride = static_cast<int64_t>(plan->own_new.heads_per_rank()) * sh.head_dim * sh.elem_bytes;
@@ -924,6 +936,8 @@ remp_status remp_kv_pack(const remp_kv_plan_t* plan, int32_t old_rank, int32_t l
     if (remp_status st = collect_slices(*plan, true, old_rank, layer_begin, layer_end, *src, staging,
                                         (flags & REMP_KV_SKIP_LOCAL) != 0, slices))
         return st;
+    if (src->layout != kLayoutNHD && !hnd_single_heads(src->layout, slices))
+        if (remp_status st = check_tile_fits(plan, plan->shape.old_block_size, "pack")) return st;
     // an empty window or cache does nothing; otherwise the tables are expanded (and their stamp
     // written) even when the rank has no slice in the window, so that later calls may reuse them
     if (layer_begin == layer_end || plan->old_live_blocks == 0) return REMP_OK;
@@ -1049,6 +1063,11 @@ remp_status remp_kv_copy_local(const remp_kv_plan_t* plan, int32_t rank, int32_t
         h.row_bytes = static_cast<uint32_t>(it.head_count * hrow);
         items.push_back(h);
     }
+    if (src->layout != kLayoutNHD || dst->layout != kLayoutNHD) {
+        if (remp_status st = check_tile_fits(plan, sh.new_block_size, "local copy")) return st;
+    }
+    if (sh.new_block_size > kMaxLocalRows)
+        return fail(REMP_E_UNSUPPORTED, "new block size above the local-copy row limit");
     if (layer_begin == layer_end || plan->new_live_blocks == 0) return REMP_OK;   // as in pack
     const WorkspaceLayout L = workspace_layout(*plan);
     char* ws = static_cast<char*>(workspace);

@@ -116,6 +116,31 @@ def test_noalloc_refusals_before_any_device_call():
     assert e.value.status_name == "REMP_E_RANGE"
 
 
+def test_tile_shape_refusals_before_any_device_call():
+    """A (block, head) tile that does not fit the head-tile kernels' LDS budget (128 rows of 256 bytes, 34816
+    bytes with the row padding) is refused by pack (ROCm pool), unpack and the local copy (HND pools) with
+    REMP_E_UNSUPPORTED before anything is enqueued: no device is touched on a machine without a GPU.  (An
+    HND pack whose slices carry one head each copies rows, not tiles, hence the ROCm pool for the pack.)"""
+    tables = synthkv.tables_from_rows(np.array([300, 129], np.int32), [[3, 0, 5], [1, 6]], 8, 128)
+    ht = rk.HostTables.of(tables)
+    plan = rk.Plan((1, 1), (1, 1), (1, 1, 128, 2, 128, 128), ht)
+    (pair,) = plan.pairs
+    dev = rk.dev_tables(0x70000000, 0x70001000, 0x70002000)
+    stage = rk.buffers([(0x50000000, pair.staging_bytes)])
+    ws, ws_bytes = 0x60000000, plan.workspace_bytes
+    src = lambda layout: rk.PoolArg([0x10000000], [0x20000000], 8, layout=layout)
+    dst = lambda layout: rk.PoolArg([0x30000000], [0x40000000], 8, layout=layout)
+    calls = {"pack": lambda: plan.pack(0, src(rk.LAYOUT_ROCM_SPLIT), dev, stage, ws, ws_bytes, None),
+             "unpack": lambda: plan.unpack(0, stage, dst(rk.LAYOUT_HND), ht, dev, ws, ws_bytes, None),
+             "local": lambda: plan.copy_local(0, src(rk.LAYOUT_HND), dev, dst(rk.LAYOUT_HND), ht, dev, ws, ws_bytes,
+                                              None)}
+    for name, call in calls.items():
+        with pytest.raises(rk.RempError) as e:
+            call()
+        assert e.value.status_name == "REMP_E_UNSUPPORTED", name
+        assert "LDS" in str(e.value), name
+
+
 def test_only_the_abi_is_exported_from_host_code():
     import subprocess
     out = subprocess.run(["nm", "-D", "--defined-only", rk._lib._LIB_PATH], capture_output=True, text=True).stdout
